@@ -24,7 +24,9 @@
  *   - s-level stochastic quantizer: r = fl(|p| * fl(s/sigma)),
  *     l = min(floor(r), s), frac = r - l, round up iff u < frac, level capped
  *     at s; the decoded value is copysign(fl(level * fl(sigma/s)), p).
- *     A zero-norm segment quantizes to level 0 everywhere.
+ *     A zero-norm segment quantizes to level 0 everywhere, and so does a
+ *     zero element (|v_i| / ||v|| = 0 gives l = 0 and round-up probability 0,
+ *     even where s/sigma overflows).
  *   - Uniforms for stochastic rounding come from Philox4x32-10 with key
  *     (lo32(seed), hi32(seed)) and counter (lo32(i>>2), m, t, hi32(i>>2));
  *     element i takes output word (i & 3) and u = (word >> 8) * 2^-24.
@@ -142,8 +144,8 @@ void oracle_qsgd_encode(int64_t n, int64_t i0, const float *p, float sigma, int3
     for (int64_t i = 0; i < n; ++i) {
         int neg = signbit(p[i]) ? 1 : 0;
         int32_t level = 0;
-        if (sigma > 0.0f) {
-            float a = fabsf(p[i]);
+        float a = fabsf(p[i]);
+        if (sigma > 0.0f && a > 0.0f) {
             float r = a * inv;
             float l = floorf(r);
             if (l > fs) l = fs;
