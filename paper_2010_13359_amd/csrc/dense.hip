@@ -1,0 +1,635 @@
+// Kernels of the dense compressors: scaled sign, s-level stochastic
+// quantizer, identity (Algorithm 2 of arXiv:2010.13359 with the compressors
+// of its Section 2.4).
+//
+// Passes over HBM per iteration:
+//   1. segment statistics: per (worker, segment) sum |p|, sum p^2 or max |p|
+//      of p = fl(fl(eta g) + e), one workgroup per piece, binary64 partials;
+//      a tiny kernel then combines the partials of each segment in piece
+//      order (deterministic) into the scale and the quantizer constants.
+//   2. the fused step: element-major; a lane owns one quad of 4 elements and
+//      walks the M workers in ascending order, encoding, writing e_t and the
+//      message, and summing p-hat in registers; then w_t = w_{t-1} - q-hat and
+//      the M evaluation points w_t - (fl(eta g) + e_t), whose right operands
+//      it kept in registers.
+#include "device.hpp"
+#include "plan.hpp"
+
+namespace dq {
+
+namespace {
+
+enum { kSign = DQGAN_SIGN, kQsgd = DQGAN_QSGD, kIdentity = DQGAN_IDENTITY };
+
+// ---------------------------------------------------------------------------
+// Pass 1: segment statistics.
+
+template <int NORM>
+__global__ __launch_bounds__(kBlock) void k_segment_partials(const float *__restrict__ G, const float *__restrict__ E,
+                                                             float eta, int64_t ld, const Piece *__restrict__ pieces,
+                                                             int32_t n_pieces, double *__restrict__ partial,
+                                                             float *__restrict__ pmax) {
+    const int pc = blockIdx.x;
+    const int m = blockIdx.y;
+    const Piece P = pieces[pc];
+    const float *g = G + static_cast<int64_t>(m) * ld;
+    const float *e = E + static_cast<int64_t>(m) * ld;
+    const int64_t lo = P.start, hi = P.start + P.len;
+    const int64_t q0 = lo >> 2, q1 = (hi + 3) >> 2;
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
+    float mx = 0.0f;
+    for (int64_t q = q0 + threadIdx.x; q < q1; q += kBlock) {
+        const f32x4 gv = ld4(g + 4 * q);
+        const f32x4 ev = ld4(e + 4 * q);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int64_t i = 4 * q + c;
+            const float p = add_rn(mul_rn(eta, elem(gv, c)), elem(ev, c));
+            const bool in = (i >= lo) && (i < hi);
+            if (NORM == DQGAN_L1) {
+                acc[c] += in ? static_cast<double>(fabsf(p)) : 0.0;
+            } else if (NORM == DQGAN_L2) {
+                const double pd = static_cast<double>(p);
+                acc[c] += in ? pd * pd : 0.0;  // the product is exact in binary64
+            } else {
+                mx = in ? fmaxf(mx, fabsf(p)) : mx;
+            }
+        }
+    }
+    __shared__ double sh[kBlock / 64];
+    __shared__ float shm[kBlock / 64];
+    double s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        s += __shfl_xor(s, o);
+        mx = fmaxf(mx, __shfl_xor(mx, o));
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        sh[wave] = s;
+        shm[wave] = mx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int64_t o = static_cast<int64_t>(m) * n_pieces + pc;
+        partial[o] = (sh[0] + sh[1]) + (sh[2] + sh[3]);
+        pmax[o] = fmaxf(fmaxf(shm[0], shm[1]), fmaxf(shm[2], shm[3]));
+    }
+}
+
+// Combine the partials of each (worker, segment) in piece order, or take the
+// caller's scales, and derive the per-segment constants: SIGN (scale, -);
+// QSGD (fl(s/sigma), fl(sigma/s)), (0, 0) for sigma = 0.  Quotients of two
+// binary32 values computed in binary64 and rounded to binary32 equal the
+// correctly rounded binary32 quotient (53 >= 2*24 + 2).
+__global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int levels, const double *__restrict__ partial,
+                                                     const float *__restrict__ pmax, int32_t n_pieces,
+                                                     const int32_t *__restrict__ seg_piece,
+                                                     const int64_t *__restrict__ off, int32_t M, int32_t n_seg,
+                                                     const float *__restrict__ scales_in, float *__restrict__ scale_out,
+                                                     float2 *__restrict__ consts) {
+    const int64_t tid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    if (tid >= static_cast<int64_t>(M) * n_seg) return;
+    const int m = static_cast<int>(tid / n_seg);
+    const int j = static_cast<int>(tid % n_seg);
+    float sc;
+    if (scales_in) {
+        sc = scales_in[tid];
+    } else if (norm == DQGAN_LINF) {
+        float mx = 0.0f;
+        for (int p = seg_piece[j]; p < seg_piece[j + 1]; ++p) mx = fmaxf(mx, pmax[static_cast<int64_t>(m) * n_pieces + p]);
+        sc = mx;
+    } else {
+        double s = 0.0;
+        for (int p = seg_piece[j]; p < seg_piece[j + 1]; ++p) s += partial[static_cast<int64_t>(m) * n_pieces + p];
+        if (norm == DQGAN_L1)
+            sc = static_cast<float>(s / static_cast<double>(off[j + 1] - off[j]));
+        else
+            sc = static_cast<float>(sqrt(s));
+    }
+    if (scale_out) scale_out[tid] = sc;
+    float2 c;
+    if (kind == kQsgd) {
+        const double sd = static_cast<double>(sc), ld = static_cast<double>(levels);
+        if (sc > 0.0f && sc <= 3.402823466e38f) {
+            c.x = static_cast<float>(ld / sd);
+            c.y = static_cast<float>(sd / ld);
+        } else {
+            c.x = 0.0f;
+            c.y = 0.0f;
+        }
+    } else {
+        c.x = sc;
+        c.y = 0.0f;
+    }
+    consts[tid] = c;
+}
+
+// ---------------------------------------------------------------------------
+// Per-quad encode of one worker row (shared by the row kernel and the fused
+// step).  Outputs: eg = fl(eta g), p-hat, e_t = fl(p - p-hat), the 4 sign bits
+// and the 4 level fields (8 bits each, packed low to high).
+
+struct QuadCodes {
+    f32x4 eg, phat, enew;
+    uint32_t sign_nib;
+    uint32_t levels;
+};
+
+template <int KIND>
+__device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, float eta, int64_t i0, int64_t d, int m,
+                                                 const int js[4], const float2 *__restrict__ crow, int s,
+                                                 uint32_t k0, uint32_t k1, uint32_t t) {
+    QuadCodes o;
+    o.sign_nib = 0u;
+    o.levels = 0u;
+    u32x4 rnd;
+    if (KIND == kQsgd) {
+        const uint64_t blk = static_cast<uint64_t>(i0) >> 2;
+        rnd = philox4x32_10(static_cast<uint32_t>(blk), static_cast<uint32_t>(m), t, static_cast<uint32_t>(blk >> 32),
+                            k0, k1);
+    }
+    const float fs = static_cast<float>(s);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float gc = elem(g, c), ec = elem(e, c);
+        const float egc = mul_rn(eta, gc);
+        const float p = add_rn(egc, ec);
+        float q = 0.0f, en = ec, egk = 0.0f;
+        uint32_t neg = 0u, level = 0u;
+        if (i0 + c < d) {
+            egk = egc;
+            neg = signbit(p) ? 1u : 0u;
+            if (KIND == kSign) {
+                const float sc = crow[js[c]].x;
+                q = neg ? -sc : sc;
+            } else if (KIND == kQsgd) {
+                const float2 cs = crow[js[c]];
+                const float a = fabsf(p);
+                if (cs.x > 0.0f && a > 0.0f) {
+                    const float r = mul_rn(a, cs.x);
+                    const float l = fminf(floorf(r), fs);
+                    const float frac = (l == fs) ? 0.0f : sub_rn(r, l);
+                    const float u = static_cast<float>(elem(rnd, c) >> 8) * 0x1.0p-24f;
+                    int lv = static_cast<int>(l) + ((u < frac) ? 1 : 0);
+                    lv = lv > s ? s : lv;
+                    level = static_cast<uint32_t>(lv);
+                }
+                q = copysignf(mul_rn(static_cast<float>(level), cs.y), p);
+            } else {
+                q = p;
+            }
+            en = sub_rn(p, q);
+        }
+        set_elem(o.eg, c, egk);
+        set_elem(o.phat, c, q);
+        set_elem(o.enew, c, en);
+        o.sign_nib |= neg << c;
+        o.levels |= level << (8 * c);
+    }
+    return o;
+}
+
+__device__ __forceinline__ void lookup_segments(const int64_t *__restrict__ off, const int32_t *__restrict__ tile_seg,
+                                                int64_t i0, int64_t d, int js[4]) {
+    const int64_t last = d - 1;
+    int j = tile_seg[i0 >> 10];
+    j = seg_from(off, j, i0 < last ? i0 : last);
+    js[0] = j;
+#pragma unroll
+    for (int c = 1; c < 4; ++c) {
+        const int64_t i = i0 + c;
+        j = seg_from(off, j, i < last ? i : last);
+        js[c] = j;
+    }
+}
+
+// Message stores for one quad of one row.
+template <int KIND, int LB>
+__device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, uint32_t *__restrict__ level_row,
+                                              float *__restrict__ val_row, int64_t q, const QuadCodes &cq) {
+    if (KIND == kSign || KIND == kQsgd) {
+        const uint32_t word = or_reduce8_to_lane4(cq.sign_nib << (4 * (q & 7)));
+        if ((q & 7) == 4) sign_row[q >> 3] = word;
+    }
+    if (KIND == kQsgd) {
+        if (LB == 8) {
+            level_row[q] = cq.levels;
+        } else {
+            const uint32_t l = cq.levels;
+            const uint16_t h = static_cast<uint16_t>((l & 0xFu) | ((l >> 4) & 0xF0u) | ((l >> 8) & 0xF00u) |
+                                                     ((l >> 12) & 0xF000u));
+            reinterpret_cast<uint16_t *>(level_row)[q] = h;
+        }
+    }
+    if (KIND == kIdentity) st4(val_row + 4 * q, cq.phat);
+}
+
+struct RowArgs {
+    float eta;
+    uint32_t t;
+    int64_t d, ld;
+    int32_t M, n_seg, s;
+    uint32_t k0, k1;
+    int64_t sign_words, level_words;  // words per row of each plane
+};
+
+// Worker side only (dqgan_compress_ef): one (quad, worker) per thread.
+template <int KIND, int LB>
+__global__ __launch_bounds__(kBlock) void k_encode_rows(const float *__restrict__ G, float *__restrict__ E,
+                                                        uint32_t *__restrict__ sign_plane,
+                                                        uint32_t *__restrict__ level_plane, float *__restrict__ val,
+                                                        const float2 *__restrict__ consts,
+                                                        const int64_t *__restrict__ off,
+                                                        const int32_t *__restrict__ tile_seg, RowArgs a) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
+    const int m = blockIdx.y;
+    const int64_t i0 = 4 * q;
+    const int64_t rb = static_cast<int64_t>(m) * a.ld;
+    int js[4];
+    lookup_segments(off, tile_seg, i0, a.d, js);
+    const f32x4 g = ld_stream(G + rb + i0);
+    const f32x4 e = ld_stream(E + rb + i0);
+    const QuadCodes cq =
+        encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg, a.s, a.k0, a.k1, a.t);
+    st_stream(E + rb + i0, cq.enew);
+    store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq);
+}
+
+// The fused step.  MT > 0: M == MT, the extrapolation operands stay in
+// registers; MT == 0: any M, the second sweep re-reads g and the new e.
+template <int KIND, int LB, int MT>
+__global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, float *__restrict__ E,
+                                                  float *__restrict__ W, float *__restrict__ WX,
+                                                  float *__restrict__ Qhat, uint32_t *__restrict__ sign_plane,
+                                                  uint32_t *__restrict__ level_plane, float *__restrict__ val,
+                                                  const float2 *__restrict__ consts, const int64_t *__restrict__ off,
+                                                  const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
+    const int64_t i0 = 4 * q;
+    const int M = MT > 0 ? MT : a.M;
+    int js[4];
+    lookup_segments(off, tile_seg, i0, a.d, js);
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    f32x4 xs[MT > 0 ? MT : 1];
+#pragma unroll(MT > 0 ? MT : 1)
+    for (int m = 0; m < M; ++m) {
+        const int64_t rb = static_cast<int64_t>(m) * a.ld;
+        const f32x4 g = ld_stream(G + rb + i0);
+        const f32x4 e = ld_stream(E + rb + i0);
+        const QuadCodes cq = encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg,
+                                               a.s, a.k0, a.k1, a.t);
+        st_stream(E + rb + i0, cq.enew);
+        store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq);
+        if (m == 0) {
+            acc = cq.phat;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) set_elem(acc, c, add_rn(elem(acc, c), elem(cq.phat, c)));
+        }
+        if (MT > 0) {
+            f32x4 x;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) set_elem(x, c, add_rn(elem(cq.eg, c), elem(cq.enew, c)));
+            xs[MT > 0 ? m : 0] = x;
+        }
+    }
+    f32x4 qh;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float sacc = elem(acc, c);
+        const float v = invM > 0.0f ? mul_rn(sacc, invM)
+                                    : static_cast<float>(static_cast<double>(sacc) / static_cast<double>(M));
+        set_elem(qh, c, v);
+    }
+    const f32x4 w = ld4(W + i0);
+    f32x4 wt;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) set_elem(wt, c, sub_rn(elem(w, c), elem(qh, c)));
+    st4(W + i0, wt);
+    if (Qhat) st4(Qhat + i0, qh);
+#pragma unroll(MT > 0 ? MT : 1)
+    for (int m = 0; m < M; ++m) {
+        const int64_t rb = static_cast<int64_t>(m) * a.ld;
+        f32x4 x;
+        if (MT > 0) {
+            x = xs[MT > 0 ? m : 0];
+        } else {
+            const f32x4 g = ld4(G + rb + i0);
+            const f32x4 en = ld4(E + rb + i0);
+#pragma unroll
+            for (int c = 0; c < 4; ++c) set_elem(x, c, add_rn(mul_rn(a.eta, elem(g, c)), elem(en, c)));
+        }
+        f32x4 wx;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) set_elem(wx, c, (i0 + c < a.d) ? sub_rn(elem(wt, c), elem(x, c)) : 0.0f);
+        st_stream(WX + rb + i0, wx);
+    }
+}
+
+// Decode one quad of one row's message to p-hat.
+template <int KIND, int LB>
+__device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_row, const uint32_t *__restrict__ level_row,
+                                             const float *__restrict__ val_row, const float2 *__restrict__ crow,
+                                             int64_t q, int64_t d, const int js[4]) {
+    const int64_t i0 = 4 * q;
+    f32x4 out = {0.0f, 0.0f, 0.0f, 0.0f};
+    if (KIND == kIdentity) {
+        const f32x4 v = ld4(val_row + i0);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) set_elem(out, c, (i0 + c < d) ? elem(v, c) : 0.0f);
+        return out;
+    }
+    const uint32_t nib = (sign_row[q >> 3] >> (4 * (q & 7))) & 0xFu;
+    uint32_t lev = 0u;
+    if (KIND == kQsgd) {
+        if (LB == 8) {
+            lev = level_row[q];
+        } else {
+            const uint32_t h = reinterpret_cast<const uint16_t *>(level_row)[q];
+            lev = (h & 0xFu) | ((h & 0xF0u) << 4) | ((h & 0xF00u) << 8) | ((h & 0xF000u) << 12);
+        }
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        if (i0 + c >= d) continue;
+        const bool neg = (nib >> c) & 1u;
+        float mag;
+        if (KIND == kSign) {
+            mag = crow[js[c]].x;
+        } else {
+            const uint32_t l = (lev >> (8 * c)) & 0xFFu;
+            mag = mul_rn(static_cast<float>(l), crow[js[c]].y);
+        }
+        set_elem(out, c, neg ? -mag : mag);
+    }
+    return out;
+}
+
+template <int KIND, int LB>
+__global__ __launch_bounds__(kBlock) void k_unpack(const uint32_t *__restrict__ sign_plane,
+                                                   const uint32_t *__restrict__ level_plane,
+                                                   const float *__restrict__ val, float *__restrict__ Phat,
+                                                   const float2 *__restrict__ consts, const int64_t *__restrict__ off,
+                                                   const int32_t *__restrict__ tile_seg, RowArgs a) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
+    const int m = blockIdx.y;
+    const int64_t rb = static_cast<int64_t>(m) * a.ld;
+    int js[4];
+    lookup_segments(off, tile_seg, 4 * q, a.d, js);
+    const f32x4 v = decode_quad<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb,
+                                          consts + static_cast<int64_t>(m) * a.n_seg, q, a.d, js);
+    st_stream(Phat + rb + 4 * q, v);
+}
+
+template <int KIND, int LB>
+__global__ __launch_bounds__(kBlock) void k_aggregate(const uint32_t *__restrict__ sign_plane,
+                                                      const uint32_t *__restrict__ level_plane,
+                                                      const float *__restrict__ val, float *__restrict__ Qhat,
+                                                      const float2 *__restrict__ consts,
+                                                      const int64_t *__restrict__ off,
+                                                      const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
+    int js[4];
+    lookup_segments(off, tile_seg, 4 * q, a.d, js);
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int m = 0; m < a.M; ++m) {
+        const int64_t rb = static_cast<int64_t>(m) * a.ld;
+        const f32x4 v = decode_quad<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb,
+                                              consts + static_cast<int64_t>(m) * a.n_seg, q, a.d, js);
+        if (m == 0) {
+            acc = v;
+        } else {
+#pragma unroll
+            for (int c = 0; c < 4; ++c) set_elem(acc, c, add_rn(elem(acc, c), elem(v, c)));
+        }
+    }
+    f32x4 qh;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float sacc = elem(acc, c);
+        set_elem(qh, c, invM > 0.0f ? mul_rn(sacc, invM)
+                                    : static_cast<float>(static_cast<double>(sacc) / static_cast<double>(a.M)));
+    }
+    st4(Qhat + 4 * q, qh);
+}
+
+__global__ __launch_bounds__(kBlock) void k_omd(const float *__restrict__ Qhat, float *__restrict__ W,
+                                                const float *__restrict__ G, const float *__restrict__ E,
+                                                float *__restrict__ WX, float eta, int64_t d, int64_t ld, int32_t M) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
+    const int64_t i0 = 4 * q;
+    const f32x4 w = ld4(W + i0);
+    const f32x4 qh = ld4(Qhat + i0);
+    f32x4 wt;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) set_elem(wt, c, (i0 + c < d) ? sub_rn(elem(w, c), elem(qh, c)) : elem(w, c));
+    st4(W + i0, wt);
+    if (!WX) return;
+    for (int m = 0; m < M; ++m) {
+        const int64_t rb = static_cast<int64_t>(m) * ld;
+        const f32x4 g = ld_stream(G + rb + i0);
+        const f32x4 e = ld_stream(E + rb + i0);
+        f32x4 wx;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float x = add_rn(mul_rn(eta, elem(g, c)), elem(e, c));
+            set_elem(wx, c, (i0 + c < d) ? sub_rn(elem(wt, c), x) : 0.0f);
+        }
+        st_stream(WX + rb + i0, wx);
+    }
+}
+
+template <int LB>
+__global__ __launch_bounds__(kBlock) void k_pack(const uint16_t *__restrict__ codes, uint32_t *__restrict__ sign_plane,
+                                                 uint32_t *__restrict__ level_plane, RowArgs a) {
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
+    const int m = blockIdx.y;
+    const int64_t i0 = 4 * q;
+    const uint2 raw = *reinterpret_cast<const uint2 *>(codes + static_cast<int64_t>(m) * a.ld + i0);
+    const uint32_t c4[4] = {raw.x & 0xFFFFu, raw.x >> 16, raw.y & 0xFFFFu, raw.y >> 16};
+    QuadCodes cq;
+    cq.sign_nib = 0u;
+    cq.levels = 0u;
+    const uint32_t fmask = LB == 8 ? 0xFFu : 0xFu;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        if (i0 + c >= a.d) continue;
+        cq.sign_nib |= ((c4[c] >> 15) & 1u) << c;
+        cq.levels |= (c4[c] & fmask) << (8 * c);
+    }
+    if (LB == 0)
+        store_message<kSign, 0>(sign_plane + m * a.sign_words, nullptr, nullptr, q, cq);
+    else
+        store_message<kQsgd, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, nullptr, q, cq);
+}
+
+RowArgs row_args(const dqgan_plan_s &P, float eta, uint32_t t) {
+    RowArgs a;
+    a.eta = eta;
+    a.t = t;
+    a.d = P.desc.d;
+    a.ld = P.desc.ld;
+    a.M = P.desc.M;
+    a.n_seg = P.desc.n_seg;
+    a.s = P.desc.levels;
+    a.k0 = static_cast<uint32_t>(P.desc.seed);
+    a.k1 = static_cast<uint32_t>(P.desc.seed >> 32);
+    a.sign_words = P.desc.ld / 32;
+    a.level_words = P.level_bits ? P.desc.ld * P.level_bits / 32 : 0;
+    return a;
+}
+
+// 1/M when M is a power of two (then x * (1/M) equals x / M exactly),
+// else 0 (the kernels divide).
+float inv_m(int M) { return (M & (M - 1)) == 0 ? 1.0f / static_cast<float>(M) : 0.0f; }
+
+template <int KIND, int LB, int MT>
+hipError_t fused_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
+                        const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    hipLaunchKernelGGL((k_fused<KIND, LB, MT>), dim3(static_cast<unsigned>(P.n_tiles)), dim3(kBlock), 0, st, G, E, W,
+                       WX, Qhat, w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a, inv_m(P.desc.M));
+    return hipGetLastError();
+}
+
+template <int KIND, int LB>
+hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
+                      const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    switch (P.desc.M) {
+        case 1: return fused_launch<KIND, LB, 1>(P, a, G, E, W, WX, w, Qhat, st);
+        case 2: return fused_launch<KIND, LB, 2>(P, a, G, E, W, WX, w, Qhat, st);
+        case 4: return fused_launch<KIND, LB, 4>(P, a, G, E, W, WX, w, Qhat, st);
+        case 8: return fused_launch<KIND, LB, 8>(P, a, G, E, W, WX, w, Qhat, st);
+        case 16: return fused_launch<KIND, LB, 16>(P, a, G, E, W, WX, w, Qhat, st);
+        case 32: return fused_launch<KIND, LB, 32>(P, a, G, E, W, WX, w, Qhat, st);
+        default: return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_segment_scales(const dqgan_plan_s &P, float eta, const float *G, const float *E,
+                                 const float *scales_in, float *scale_out, hipStream_t st) {
+    const dqgan_desc &D = P.desc;
+    if (!scales_in) {
+        const dim3 grid(static_cast<unsigned>(P.n_pieces), static_cast<unsigned>(D.M));
+        if (D.norm == DQGAN_L1)
+            hipLaunchKernelGGL(k_segment_partials<DQGAN_L1>, grid, dim3(kBlock), 0, st, G, E, eta, D.ld, P.d_pieces,
+                               P.n_pieces, P.d_partial, P.d_pmax);
+        else if (D.norm == DQGAN_L2)
+            hipLaunchKernelGGL(k_segment_partials<DQGAN_L2>, grid, dim3(kBlock), 0, st, G, E, eta, D.ld, P.d_pieces,
+                               P.n_pieces, P.d_partial, P.d_pmax);
+        else
+            hipLaunchKernelGGL(k_segment_partials<DQGAN_LINF>, grid, dim3(kBlock), 0, st, G, E, eta, D.ld,
+                               P.d_pieces, P.n_pieces, P.d_partial, P.d_pmax);
+        hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    const int64_t n = static_cast<int64_t>(D.M) * D.n_seg;
+    hipLaunchKernelGGL(k_finalize, dim3(static_cast<unsigned>((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, st, D.kind,
+                       D.norm, D.levels, P.d_partial, P.d_pmax, P.n_pieces, P.d_seg_piece, P.d_off, D.M, D.n_seg,
+                       scales_in, scale_out, P.d_consts);
+    return hipGetLastError();
+}
+
+hipError_t launch_consts_from_scales(const dqgan_plan_s &P, const float *scales, hipStream_t st) {
+    return launch_segment_scales(P, 0.0f, nullptr, nullptr, scales, nullptr, st);
+}
+
+hipError_t launch_encode(const dqgan_plan_s &P, float eta, uint32_t t, const float *G, float *E, const dqgan_wire &w,
+                         hipStream_t st) {
+    const RowArgs a = row_args(P, eta, t);
+    const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
+    const int kind = P.desc.kind;
+    if (kind == kSign)
+        hipLaunchKernelGGL((k_encode_rows<kSign, 0>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
+    else if (kind == kQsgd && P.level_bits == 8)
+        hipLaunchKernelGGL((k_encode_rows<kQsgd, 8>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
+    else if (kind == kQsgd)
+        hipLaunchKernelGGL((k_encode_rows<kQsgd, 4>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
+    else
+        hipLaunchKernelGGL((k_encode_rows<kIdentity, 0>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_fused_dense(const dqgan_plan_s &P, float eta, uint32_t t, const float *G, float *E, float *W,
+                              float *WX, const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    const RowArgs a = row_args(P, eta, t);
+    const int kind = P.desc.kind;
+    if (kind == kSign) return fused_by_m<kSign, 0>(P, a, G, E, W, WX, w, Qhat, st);
+    if (kind == kQsgd && P.level_bits == 8) return fused_by_m<kQsgd, 8>(P, a, G, E, W, WX, w, Qhat, st);
+    if (kind == kQsgd) return fused_by_m<kQsgd, 4>(P, a, G, E, W, WX, w, Qhat, st);
+    return fused_by_m<kIdentity, 0>(P, a, G, E, W, WX, w, Qhat, st);
+}
+
+hipError_t launch_pack(const dqgan_plan_s &P, const uint16_t *codes, const dqgan_wire &w, hipStream_t st) {
+    const RowArgs a = row_args(P, 0.0f, 0);
+    const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
+    if (P.desc.kind == kSign)
+        hipLaunchKernelGGL(k_pack<0>, grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+    else if (P.level_bits == 8)
+        hipLaunchKernelGGL(k_pack<8>, grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+    else
+        hipLaunchKernelGGL(k_pack<4>, grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpack_dense(const dqgan_plan_s &P, const dqgan_wire &w, float *Phat, hipStream_t st) {
+    const RowArgs a = row_args(P, 0.0f, 0);
+    const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
+    const int kind = P.desc.kind;
+    if (kind != kIdentity) {
+        hipError_t err = launch_consts_from_scales(P, w.scale, st);
+        if (err != hipSuccess) return err;
+    }
+    if (kind == kSign)
+        hipLaunchKernelGGL((k_unpack<kSign, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
+                           P.d_off, P.d_tile_seg, a);
+    else if (kind == kQsgd && P.level_bits == 8)
+        hipLaunchKernelGGL((k_unpack<kQsgd, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
+                           P.d_off, P.d_tile_seg, a);
+    else if (kind == kQsgd)
+        hipLaunchKernelGGL((k_unpack<kQsgd, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
+                           P.d_off, P.d_tile_seg, a);
+    else
+        hipLaunchKernelGGL((k_unpack<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_aggregate_dense(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    const RowArgs a = row_args(P, 0.0f, 0);
+    const dim3 grid(static_cast<unsigned>(P.n_tiles));
+    const int kind = P.desc.kind;
+    const float im = inv_m(P.desc.M);
+    if (kind != kIdentity) {
+        hipError_t err = launch_consts_from_scales(P, w.scale, st);
+        if (err != hipSuccess) return err;
+    }
+    if (kind == kSign)
+        hipLaunchKernelGGL((k_aggregate<kSign, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    else if (kind == kQsgd && P.level_bits == 8)
+        hipLaunchKernelGGL((k_aggregate<kQsgd, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    else if (kind == kQsgd)
+        hipLaunchKernelGGL((k_aggregate<kQsgd, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    else
+        hipLaunchKernelGGL((k_aggregate<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    return hipGetLastError();
+}
+
+hipError_t launch_omd(const dqgan_plan_s &P, float eta, const float *Qhat, float *W, const float *G, const float *E,
+                      float *WX, hipStream_t st) {
+    hipLaunchKernelGGL(k_omd, dim3(static_cast<unsigned>(P.n_tiles)), dim3(kBlock), 0, st, Qhat, W, G, E, WX, eta,
+                       P.desc.d, P.desc.ld, P.desc.M);
+    return hipGetLastError();
+}
+
+}  // namespace dq

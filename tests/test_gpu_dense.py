@@ -1,0 +1,204 @@
+"""GPU parity of the dense compressors (scaled sign, s-level quantizer,
+identity) through the C ABI, against the oracle on the same inputs.
+
+Teacher-forced: the oracle recomputes the iteration from the same pre-step
+state with the GPU's segment scales; every message bit and every binary32
+output must be identical.  The scales themselves must agree with the
+oracle's own within 1e-5 relative."""
+import numpy as np
+import pytest
+
+from gpu_common import GpuState, assert_same, compare_step, inputs, to_dev, u32
+import synth
+from synth.configs import custom
+
+pytestmark = pytest.mark.gpu
+
+CASES = {
+    # name: workload
+    "sign_2seg_m4": lambda: custom(d=5000, M=4, kind="sign", seg_offsets=[0, 1234, 5000], eta=1e-2, seed=1),
+    "sign_tiny_segs_m2": lambda: custom(d=100, M=2, kind="sign", seg_offsets=[0, 1, 2, 3, 50, 99, 100], eta=1e-2,
+                                        seed=2),
+    "sign_d1_m1": lambda: custom(d=1, M=1, kind="sign", eta=1e-2, seed=3),
+    "sign_d33_m3": lambda: custom(d=33, M=3, kind="sign", seg_offsets=[0, 31, 33], eta=1e-2, seed=4),
+    "sign_c0": lambda: synth.get(0),
+    "qsgd15_l2_m4": lambda: custom(d=5000, M=4, kind="qsgd", levels=15, seg_offsets=[0, 1234, 5000], eta=1e-2,
+                                   seed=5),
+    "qsgd15_l2_m32_many": lambda: custom(d=70001, M=32, kind="qsgd", levels=15,
+                                         seg_offsets=[0, 64, 65, 1000, 4097, 30000, 65536, 70001], eta=1e-2, seed=6),
+    "qsgd15_l2_m5_generic": lambda: custom(d=9000, M=5, kind="qsgd", levels=15, seg_offsets=[0, 4500, 9000],
+                                           eta=1e-2, seed=7),
+    "qsgd15_linf_m8": lambda: custom(d=20000, M=8, kind="qsgd", levels=15, norm="linf",
+                                     seg_offsets=[0, 7, 19999, 20000], eta=1e-2, seed=8),
+    "qsgd255_l2_m8": lambda: custom(d=3001, M=8, kind="qsgd", levels=255, seg_offsets=[0, 3001], eta=1e-2, seed=9),
+    "qsgd255_linf_m16": lambda: custom(d=40000, M=16, kind="qsgd", levels=255, norm="linf",
+                                       seg_offsets=[0, 100, 40000], eta=1e-2, seed=10),
+    "qsgd255_m64_generic": lambda: custom(d=2048, M=64, kind="qsgd", levels=255, eta=1e-2, seed=11),
+    "identity_m2": lambda: custom(d=4097, M=2, kind="identity", eta=1e-2, seed=12),
+    "identity_m1": lambda: custom(d=1500, M=1, kind="identity", eta=1e-2, seed=13),
+}
+
+
+def _oracle(w, G, E, W, scales_in=None, t=1):
+    from oracle import oracle as orc
+    return orc.step(w.as_dict(), np.float32(w.eta), t, G, E.copy(), W.copy(), scales_in=scales_in)
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_fused_step_teacher_forced(name):
+    w = CASES[name]()
+    G, E, W = inputs(w)
+    print("case", name, "d", w.d, "M", w.M, flush=True)
+    s = GpuState(w, G, E, W)
+    s.fused(1)
+    gpu = s.host()
+    s.close()
+    scales = gpu.get("scale")
+    own = _oracle(w, G, E, W)
+    if scales is not None:
+        np.testing.assert_allclose(scales, own["scale"], rtol=1e-5, atol=0)
+    ref = _oracle(w, G, E, W, scales_in=scales)
+    compare_step(w, gpu, ref)
+    # padding of E and W is preserved
+    assert np.array_equal(gpu["E"][:, w.d:], E[:, w.d:]) and np.array_equal(gpu["W"][w.d:], W[w.d:])
+
+
+@pytest.mark.parametrize("name", sorted(CASES))
+def test_unfused_equals_fused(name):
+    """dqgan_compress_ef + dqgan_aggregate + dqgan_omd_step give the fused
+    step's results bit for bit."""
+    w = CASES[name]()
+    G, E, W = inputs(w)
+    a = GpuState(w, G, E, W)
+    a.fused(2)
+    fa = a.host()
+    a.close()
+    b = GpuState(w, G, E, W)
+    b.unfused(2)
+    fb = b.host()
+    b.close()
+    compare_step(w, fa, fb)
+
+
+@pytest.mark.parametrize("name", ["sign_2seg_m4", "qsgd15_l2_m4", "qsgd255_l2_m8", "qsgd15_l2_m32_many",
+                                  "identity_m2", "sign_tiny_segs_m2"])
+def test_unpack_matches_oracle_decode(name):
+    """The server's decode of the message (dqgan_unpack) equals the oracle's
+    decode of the same message planes."""
+    import torch
+    from oracle import oracle as orc
+    w = CASES[name]()
+    G, E, W = inputs(w)
+    s = GpuState(w, G, E, W)
+    s.dq.compress_ef(s.plan, w.eta, 3, s.G, s.E, None, s.wire)
+    Ph = torch.full((w.M, w.ld), float("nan"), dtype=torch.float32, device=s.G.device)
+    s.dq.unpack(s.plan, s.wire, Ph)
+    torch.cuda.synchronize()
+    got = Ph.cpu().numpy()
+    out = s.host()
+    s.close()
+    b = {255: 8, 15: 4}.get(w.levels, 0)
+    for m in range(w.M):
+        if w.kind == "identity":
+            exp = out["val"][m, :w.d]
+        else:
+            signs = orc.unpack_bits(out["sign"][m], 1, w.d)
+            levels = orc.unpack_bits(out["level"][m], b, w.d) if b else np.zeros(w.d, np.uint16)
+            exp = np.empty(w.d, np.float32)
+            for j in range(w.n_seg):
+                a0, a1 = w.seg_offsets[j], w.seg_offsets[j + 1]
+                exp[a0:a1] = orc.decode_segment(w.kind, signs[a0:a1], levels[a0:a1], out["scale"][m, j], w.levels)
+        assert_same("phat row %d" % m, got[m, :w.d], exp)
+        assert np.all(got[m, w.d:] == 0)
+
+
+@pytest.mark.parametrize("kind,levels", [("sign", 0), ("qsgd", 15), ("qsgd", 255)])
+def test_pack_matches_oracle(kind, levels):
+    import torch
+    from oracle import oracle as orc
+    w = custom(d=10007, M=3, kind=kind, levels=levels, seg_offsets=[0, 5000, 10007], seed=14)
+    rng = np.random.default_rng(1)
+    smax = levels if levels else 0
+    lv = rng.integers(0, smax + 1, (w.M, w.ld)).astype(np.uint16)
+    sg = rng.integers(0, 2, (w.M, w.ld)).astype(np.uint16)
+    codes = (sg << 15) | lv
+    scales = rng.uniform(0.1, 1, (w.M, w.n_seg)).astype(np.float32)
+    G, E, W = inputs(w)
+    s = GpuState(w, G, E, W)
+    ct = torch.from_numpy(codes.view(np.int16)).to(s.G.device)
+    st = to_dev(scales)
+    s.dq.pack(s.plan, ct, st, s.wire)
+    torch.cuda.synchronize()
+    out = s.host()
+    s.close()
+    b = {255: 8, 15: 4}.get(levels, 0)
+    for m in range(w.M):
+        exp_s = orc.pack_bits(sg[m, :w.d], 1, w.ld // 32)
+        assert_same("sign words", out["sign"][m], exp_s)
+        if b:
+            exp_l = orc.pack_bits(lv[m, :w.d], b, w.ld * b // 32)
+            assert_same("level words", out["level"][m], exp_l)
+    assert_same("scales", out["scale"], scales)
+
+
+def test_zero_segment_quantizes_to_zero():
+    """A segment whose p is identically zero has sigma = 0: every level is 0,
+    p-hat = 0 and e = p (the oracle's reading of the undefined case)."""
+    w = custom(d=3000, M=4, kind="qsgd", levels=15, seg_offsets=[0, 1000, 3000], eta=1e-2, seed=15)
+    G, E, W = inputs(w)
+    G[:, :1000] = 0.0
+    E[:, :1000] = 0.0
+    E[1, 5] = -0.0
+    s = GpuState(w, G, E, W)
+    s.fused(1)
+    gpu = s.host()
+    s.close()
+    assert np.all(gpu["scale"][:, 0] == 0)
+    ref = _oracle(w, G, E, W, scales_in=gpu["scale"])
+    compare_step(w, gpu, ref)
+
+
+def test_deterministic():
+    w = CASES["qsgd15_l2_m32_many"]()
+    G, E, W = inputs(w)
+    outs = []
+    for _ in range(2):
+        s = GpuState(w, G, E, W)
+        s.fused(4)
+        outs.append(s.host())
+        s.close()
+    for k in outs[0]:
+        assert np.array_equal(outs[0][k].view(np.uint32), outs[1][k].view(np.uint32)), k
+
+
+@pytest.mark.parametrize("index,steps", [(0, 10), (1, 12)])
+def test_free_running_configs(index, steps):
+    """Several iterations on each side's own state (gradients are inputs).
+    Every binary32 output within 1e-5 relative of the operand magnitude of its
+    last operation; the scaled sign has no stochastic rounding, so the states
+    are expected to stay identical."""
+    from oracle import oracle as orc
+    from gpu_common import rel_close
+    w = synth.get(index)
+    W0 = synth.init_params_np(w)
+    E0 = np.zeros((w.M, w.ld), np.float32)
+    s = GpuState(w, synth.gradients_np(w, 0), E0, W0)
+    E_r, W_r = E0.copy(), W0.copy()
+    exact = 0
+    for t in range(1, steps + 1):
+        G = synth.gradients_np(w, t)
+        s.G.copy_(to_dev(G))
+        s.fused(t)
+        d = w.d
+        P = np.abs(np.float32(w.eta) * G[:, :d]) + np.abs(E_r[:, :d])  # |p| with e_{t-1}
+        W_prev = W_r[:d].copy()
+        ref = orc.step(w.as_dict(), np.float32(w.eta), t, G, E_r, W_r)
+        gpu = s.host()
+        X = np.abs(np.float32(w.eta) * G[:, :d]) + np.abs(E_r[:, :d])  # |eta g + e_t|
+        rel_close("E", gpu["E"][:, :d], ref["E"][:, :d], tau=P + 1e-30)
+        rel_close("W", gpu["W"][:d], ref["W"][:d], tau=np.abs(W_prev) + np.abs(ref["qhat"][:d]) + 1e-30)
+        rel_close("WX", gpu["WX"][:, :d], ref["WX"][:, :d], tau=np.abs(W_r[None, :d]) + X + 1e-30)
+        rel_close("scale", gpu["scale"], ref["scale"], tau=1e-30)
+        exact += int(np.array_equal(gpu["E"][:, :d], ref["E"][:, :d]))
+    s.close()
+    print("steps with identical residuals: %d of %d" % (exact, steps))
