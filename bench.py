@@ -1,0 +1,212 @@
+"""Benchmark of the fused DQGAN iteration (Algorithm 2 of arXiv:2010.13359)
+on one MI355X.
+
+One step = one full iteration over all M workers: EF accumulate, compress,
+pack, EF residual, server average, OMD update and the M extrapolated points,
+as the two passes of the library (dqgan_step_scales, dqgan_step_apply).
+Inputs (gradients, residuals, parameters) are resident in HBM before the timed
+region; two gradient batches alternate between steps.
+
+Prints one JSON line.  `value` is gradient GB/s = M * d * 4 bytes / step time.
+`roofline` is the dominant kernel (the apply pass) against the 8 TB/s HBM
+peak, with its algorithmic bytes per launch; `step_roofline` is the same for
+the whole step.  `cpu_baseline` is the oracle (single-threaded C) on a
+bounded sample of the same workload.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+"""
+import argparse
+import hashlib
+import glob
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "GB/s of gradient processed per fused compress+EF+aggregate+OMD step; % HBM peak"
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2010_13359_amd", "csrc", "*"))):
+        with open(p, "rb") as f:
+            h.update(os.path.basename(p).encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def wire_bits(w):
+    if w.kind == "sign":
+        return 1.0
+    if w.kind == "qsgd":
+        return 1.0 + (8 if w.levels == 255 else 4)
+    if w.kind == "topk":
+        return 64.0 * w.k / w.d
+    return 32.0
+
+
+def algorithmic_bytes(w):
+    """Bytes the iteration must move at minimum: per (worker, element) read g,
+    read and write e, write the evaluation point, write the message; per
+    element read and write w; per (worker, segment) the scale."""
+    per_mi = 16.0 + wire_bits(w) / 8.0
+    return w.M * w.d * per_mi + 8.0 * w.d + 4.0 * w.M * w.n_seg
+
+
+def workload_label(w):
+    comp = {"sign": "scaled sign (L1 mean)", "qsgd": "s-level quantizer s=%d %s" % (w.levels, w.norm.upper()),
+            "topk": "top-k k=%d" % w.k, "identity": "identity"}[w.kind]
+    return "C%d %s: d=%d, M=%d workers, %s, %d segments, eta=%g" % (w.index, w.name, w.d, w.M, comp, w.n_seg, w.eta)
+
+
+def traffic_record(kernel_key):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as f:
+            rec = json.load(f).get(kernel_key)
+    except (ValueError, OSError):
+        return None
+    if not rec or rec.get("source_hash") != source_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline(w, target_elems=4_000_000):
+    """The oracle on the first segments of the workload (all M workers),
+    timed on this host; single thread."""
+    import numpy as np
+    import synth
+    from synth.configs import custom
+    from oracle import oracle as orc
+    offs = [o for o in w.seg_offsets if o <= target_elems]
+    if len(offs) < 2:
+        offs = [0, min(w.d, target_elems)]
+    n = offs[-1]
+    nseg = len(offs) - 1
+    sub = custom(d=n, M=w.M, kind=w.kind, levels=w.levels, k=max(1, w.k * n // w.d) if w.k else 0,
+                 seg_offsets=offs if w.kind != "topk" else None, norm=w.norm if w.kind in ("sign", "qsgd") else None,
+                 eta=w.eta, seed=w.seed, law=w.law, group_scale=w.group_scale[:nseg])
+    G = synth.gradients_np(sub, 1)
+    E = np.zeros((sub.M, sub.ld), np.float32)
+    W = synth.init_params_np(sub)
+    orc.lib()
+    t0 = time.perf_counter()
+    orc.step(sub.as_dict(), np.float32(sub.eta), 1, G, E, W)
+    dt = time.perf_counter() - t0
+    gbs = sub.M * sub.d * 4 / dt / 1e9
+    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "one full iteration over the first %d segments (d=%d of %d, all %d workers), "
+                      "%.1f s, single-threaded C oracle; host reports %d CPUs" % (nseg, sub.d, w.d, w.M, dt,
+                                                                                 os.cpu_count() or 0)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, help="workload index C0..C4 (default C3)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain device copy of 1 GiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
+              "one batched matrix on a single device)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+    from paper_2010_13359_amd import dqgan
+
+    w = synth.get(args.config)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    print("bench: workload %s" % workload_label(w), file=sys.stderr, flush=True)
+    plan = dqgan.Plan.from_workload(w)
+    Gs = [synth.gradients(w, t, device=dev) for t in (1, 2)]
+    E = torch.zeros((w.M, w.ld), dtype=torch.float32, device=dev)
+    W = synth.init_params(w, device=dev)
+    WX = torch.empty((w.M, w.ld), dtype=torch.float32, device=dev)
+    wire = plan.new_wire(dev)
+    torch.cuda.synchronize()
+
+    def one(t, ev=None):
+        G = Gs[t % 2]
+        if ev:
+            ev[0].record()
+        dqgan.step_scales(plan, w.eta, G, E, wire)
+        if ev:
+            ev[1].record()
+        dqgan.step_apply(plan, w.eta, t, G, E, W, WX, wire)
+        if ev:
+            ev[2].record()
+
+    for t in range(1, args.warmup + 1):
+        one(t)
+    torch.cuda.synchronize()
+    if args.copy_calibration:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record()
+    for k in range(args.steps):
+        one(args.warmup + 1 + k, evs[k])
+    stop.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    total_ms = start.elapsed_time(stop)
+    scales_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    apply_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    ms_step = total_ms / args.steps
+    grad_bytes = w.M * w.d * 4.0
+    value = grad_bytes / (ms_step * 1e-3) / 1e9
+    b_alg = algorithmic_bytes(w)
+    t_apply = sum(apply_ms) / len(apply_ms)
+    t_scales = sum(scales_ms) / len(scales_ms)
+    achieved = b_alg / (t_apply * 1e-3) / 1e9
+    step_ach = b_alg / (ms_step * 1e-3) / 1e9
+    kernel_key = "apply_C%d" % w.index
+    traffic = traffic_record(kernel_key)
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": workload_label(w), "d": w.d, "M": w.M, "compressor": w.kind, "levels": w.levels,
+                   "k": w.k, "segments": w.n_seg, "parallelism": "single GPU; M workers as rows"},
+        "roofline": {"bound": "hbm", "kernel": "dqgan_step_apply (fused encode+EF+aggregate+OMD pass)",
+                     "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": b_alg, "ms_per_launch": round(t_apply, 4)},
+        "step_roofline": {"achieved": round(step_ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                          "frac": round(step_ach / HBM_PEAK_GBS, 4), "ms_scales_pass": round(t_scales, 4),
+                          "ms_apply_pass": round(t_apply, 4)},
+        "hbm_pct_of_peak": round(100 * step_ach / HBM_PEAK_GBS, 2),
+        "wall_s_timed": round(t_wall, 3),
+    }
+    plan.close()
+    del Gs, E, W, WX, wire
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("bench: timing the oracle on a sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

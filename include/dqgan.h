@@ -180,6 +180,21 @@ dqgan_status dqgan_omd_step(dqgan_plan plan, float eta, const float *Qhat, float
 dqgan_status dqgan_step_fused(dqgan_plan plan, float eta, uint32_t t, const float *G, float *E, float *W,
                               float *WX, const dqgan_wire *out, float *Qhat, void *stream);
 
+/* The two passes of dqgan_step_fused, for callers that schedule or time them
+ * separately.  dqgan_step_scales reads G and E (e_{t-1}) once and computes
+ * what the compressor must know about the whole of each worker's vector
+ * before it can encode any element: the segment scales (SIGN, QSGD; written
+ * to out->scale) or the selection threshold (TOPK).  dqgan_step_apply then
+ * runs the fused iteration with that state, which the plan holds in its
+ * scratch: the two calls must be issued in this order on one stream with the
+ * same G and E and no other call on the plan in between.  The arguments mean
+ * what they mean for dqgan_step_fused; dqgan_step_scales then
+ * dqgan_step_apply equals dqgan_step_fused bit for bit. */
+dqgan_status dqgan_step_scales(dqgan_plan plan, float eta, const float *G, const float *E, const dqgan_wire *out,
+                               void *stream);
+dqgan_status dqgan_step_apply(dqgan_plan plan, float eta, uint32_t t, const float *G, float *E, float *W, float *WX,
+                              const dqgan_wire *out, float *Qhat, void *stream);
+
 /* Static text for a status code. */
 const char *dqgan_status_string(dqgan_status status);
 

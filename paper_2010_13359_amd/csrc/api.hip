@@ -291,6 +291,35 @@ dqgan_status dqgan_omd_step(dqgan_plan P, float eta, const float *Qhat, float *W
     return from_hip(dq::launch_omd(*P, eta, Qhat, W, G, E, WX, static_cast<hipStream_t>(stream)));
 }
 
+dqgan_status dqgan_step_scales(dqgan_plan P, float eta, const float *G, const float *E, const dqgan_wire *out,
+                               void *stream) {
+    if (!P) return DQGAN_EINVAL;
+    DQ_TRY(need(G));
+    DQ_TRY(need(E));
+    DQ_TRY(check_wire(P, out, true));
+    DQ_TRY(check_current_device(P));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int kind = P->desc.kind;
+    if (kind == DQGAN_TOPK) return from_hip(dq::launch_topk_select(*P, eta, G, E, st));
+    if (kind == DQGAN_IDENTITY) return DQGAN_OK;
+    return from_hip(dq::launch_segment_scales(*P, eta, G, E, nullptr, out->scale, st));
+}
+
+dqgan_status dqgan_step_apply(dqgan_plan P, float eta, uint32_t t, const float *G, float *E, float *W, float *WX,
+                              const dqgan_wire *out, float *Qhat, void *stream) {
+    if (!P) return DQGAN_EINVAL;
+    DQ_TRY(need(G));
+    DQ_TRY(need(E));
+    DQ_TRY(need(W));
+    DQ_TRY(need(WX));
+    DQ_TRY(optional(Qhat));
+    DQ_TRY(check_wire(P, out, true));
+    DQ_TRY(check_current_device(P));
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (P->desc.kind == DQGAN_TOPK) return from_hip(dq::launch_topk_apply(*P, eta, G, E, W, WX, *out, Qhat, st));
+    return from_hip(dq::launch_fused_dense(*P, eta, t, G, E, W, WX, *out, Qhat, st));
+}
+
 dqgan_status dqgan_step_fused(dqgan_plan P, float eta, uint32_t t, const float *G, float *E, float *W, float *WX,
                               const dqgan_wire *out, float *Qhat, void *stream) {
     if (!P) return DQGAN_EINVAL;
@@ -303,7 +332,11 @@ dqgan_status dqgan_step_fused(dqgan_plan P, float eta, uint32_t t, const float *
     DQ_TRY(check_current_device(P));
     hipStream_t st = static_cast<hipStream_t>(stream);
     const int kind = P->desc.kind;
-    if (kind == DQGAN_TOPK) return from_hip(dq::launch_topk_fused(*P, eta, G, E, W, WX, *out, Qhat, st));
+    if (kind == DQGAN_TOPK) {
+        hipError_t e = dq::launch_topk_select(*P, eta, G, E, st);
+        if (e != hipSuccess) return DQGAN_EHIP;
+        return from_hip(dq::launch_topk_apply(*P, eta, G, E, W, WX, *out, Qhat, st));
+    }
     if (kind != DQGAN_IDENTITY) {
         hipError_t e = dq::launch_segment_scales(*P, eta, G, E, nullptr, out->scale, st);
         if (e != hipSuccess) return DQGAN_EHIP;

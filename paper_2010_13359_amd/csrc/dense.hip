@@ -268,11 +268,12 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
     const int64_t i0 = 4 * q;
     const int M = MT > 0 ? MT : a.M;
+    constexpr int kUnroll = MT > 0 ? MT : 1;
     int js[4];
     lookup_segments(off, tile_seg, i0, a.d, js);
     f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
     f32x4 xs[MT > 0 ? MT : 1];
-#pragma unroll(MT > 0 ? MT : 1)
+#pragma unroll kUnroll
     for (int m = 0; m < M; ++m) {
         const int64_t rb = static_cast<int64_t>(m) * a.ld;
         const f32x4 g = ld_stream(G + rb + i0);
@@ -308,7 +309,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
     for (int c = 0; c < 4; ++c) set_elem(wt, c, sub_rn(elem(w, c), elem(qh, c)));
     st4(W + i0, wt);
     if (Qhat) st4(Qhat + i0, qh);
-#pragma unroll(MT > 0 ? MT : 1)
+#pragma unroll kUnroll
     for (int m = 0; m < M; ++m) {
         const int64_t rb = static_cast<int64_t>(m) * a.ld;
         f32x4 x;

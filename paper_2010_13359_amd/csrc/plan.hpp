@@ -69,7 +69,8 @@ hipError_t topk_alloc(dqgan_plan_s &P);
 void topk_free(dqgan_plan_s &P);
 hipError_t launch_topk_compress(const dqgan_plan_s &P, float eta, const float *G, float *E, const dqgan_wire &w,
                                 hipStream_t st);
-hipError_t launch_topk_fused(const dqgan_plan_s &P, float eta, const float *G, float *E, float *W, float *WX,
+hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, const float *E, hipStream_t st);
+hipError_t launch_topk_apply(const dqgan_plan_s &P, float eta, const float *G, float *E, float *W, float *WX,
                              const dqgan_wire &w, float *Qhat, hipStream_t st);
 hipError_t launch_topk_unpack(const dqgan_plan_s &P, const dqgan_wire &w, float *Phat, hipStream_t st);
 hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st);

@@ -9,7 +9,10 @@ void topk_free(dqgan_plan_s &) {}
 hipError_t launch_topk_compress(const dqgan_plan_s &, float, const float *, float *, const dqgan_wire &, hipStream_t) {
     return hipErrorNotSupported;
 }
-hipError_t launch_topk_fused(const dqgan_plan_s &, float, const float *, float *, float *, float *, const dqgan_wire &,
+hipError_t launch_topk_select(const dqgan_plan_s &, float, const float *, const float *, hipStream_t) {
+    return hipErrorNotSupported;
+}
+hipError_t launch_topk_apply(const dqgan_plan_s &, float, const float *, float *, float *, float *, const dqgan_wire &,
                              float *, hipStream_t) {
     return hipErrorNotSupported;
 }

@@ -21,7 +21,8 @@ NORMS = {"none": NORM_NONE, "l1": L1, "l2": L2, "linf": LINF}
 OK, EINVAL, EALIGN, ENOMEM, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
 
 EXPORTS = ("dqgan_plan_create", "dqgan_plan_destroy", "dqgan_wire_bytes", "dqgan_compress_ef", "dqgan_pack",
-           "dqgan_unpack", "dqgan_aggregate", "dqgan_omd_step", "dqgan_step_fused", "dqgan_status_string")
+           "dqgan_unpack", "dqgan_aggregate", "dqgan_omd_step", "dqgan_step_fused", "dqgan_step_scales",
+           "dqgan_step_apply", "dqgan_status_string")
 
 
 class DqganError(RuntimeError):
@@ -67,6 +68,8 @@ def load():
     L.dqgan_aggregate.argtypes = [P, ctypes.POINTER(WireStruct), P, P]
     L.dqgan_omd_step.argtypes = [P, f32, P, P, P, P, P, P]
     L.dqgan_step_fused.argtypes = [P, f32, u32, P, P, P, P, ctypes.POINTER(WireStruct), P, P]
+    L.dqgan_step_scales.argtypes = [P, f32, P, P, ctypes.POINTER(WireStruct), P]
+    L.dqgan_step_apply.argtypes = [P, f32, u32, P, P, P, P, ctypes.POINTER(WireStruct), P, P]
     L.dqgan_status_string.argtypes = [i32]
     L.dqgan_status_string.restype = ctypes.c_char_p
     for name in EXPORTS:
@@ -193,5 +196,18 @@ def omd_step(plan, eta, Qhat, W, G, E, WX, stream=None):
 def step_fused(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
     ws = wire.struct()
     _check("dqgan_step_fused", load().dqgan_step_fused(plan.handle, ctypes.c_float(eta), t, _ptr(G), _ptr(E),
+                                                       _ptr(W), _ptr(WX), ctypes.byref(ws), _ptr(Qhat),
+                                                       _stream(stream)))
+
+
+def step_scales(plan, eta, G, E, wire, stream=None):
+    ws = wire.struct()
+    _check("dqgan_step_scales", load().dqgan_step_scales(plan.handle, ctypes.c_float(eta), _ptr(G), _ptr(E),
+                                                         ctypes.byref(ws), _stream(stream)))
+
+
+def step_apply(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
+    ws = wire.struct()
+    _check("dqgan_step_apply", load().dqgan_step_apply(plan.handle, ctypes.c_float(eta), t, _ptr(G), _ptr(E),
                                                        _ptr(W), _ptr(WX), ctypes.byref(ws), _ptr(Qhat),
                                                        _stream(stream)))

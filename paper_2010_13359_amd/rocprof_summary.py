@@ -1,0 +1,81 @@
+"""Summarize a rocprofv3 results database (rocpd SQLite): per kernel, the
+dispatch count and duration statistics, and for counter runs the mean value of
+each counter per dispatch.
+
+    python -m paper_2010_13359_amd.rocprof_summary RESULTS.db [--counters]
+"""
+import argparse
+import re
+import sqlite3
+import sys
+
+
+def short_name(name):
+    """'void ns::k_fused<1, 4, 32>(float const*, ...)' -> 'k_fused<1, 4, 32>'."""
+    s = re.sub(r"^void\s+", "", name).replace("(anonymous namespace)", "anon")
+    depth, cut, last_sep = 0, len(s), 0
+    for i, ch in enumerate(s):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+        elif ch == ":" and depth == 0 and s[i:i + 2] == "::":
+            last_sep = i + 2
+    s = s[last_sep:cut]
+    return s if len(s) <= 90 else s[:87] + "..."
+
+
+def kernel_stats(db):
+    con = sqlite3.connect(db)
+    rows = con.execute("select name, duration from kernels").fetchall()
+    agg = {}
+    for name, dur in rows:
+        key = short_name(name)
+        a = agg.setdefault(key, [])
+        a.append(float(dur))
+    out = []
+    for k, v in agg.items():
+        v.sort()
+        out.append((k, len(v), sum(v) / len(v) / 1e3, v[len(v) // 2] / 1e3, v[0] / 1e3, v[-1] / 1e3, sum(v) / 1e3))
+    out.sort(key=lambda r: -r[6])
+    return out
+
+
+def counter_stats(db):
+    con = sqlite3.connect(db)
+    rows = con.execute("select kernel_name, counter_name, dispatch_id, value from counters_collection").fetchall()
+    per = {}
+    for name, ctr, disp, val in rows:
+        key = (short_name(name), ctr)
+        per.setdefault(key, {}).setdefault(disp, 0.0)
+        per[key][disp] += float(val)
+    out = []
+    for (k, ctr), d in per.items():
+        vals = list(d.values())
+        out.append((k, ctr, len(vals), sum(vals) / len(vals)))
+    out.sort()
+    return out
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    ap.add_argument("db")
+    ap.add_argument("--counters", action="store_true")
+    a = ap.parse_args(argv)
+    if a.counters:
+        print("%-60s %-12s %8s %16s" % ("kernel", "counter", "calls", "mean/dispatch"))
+        for k, ctr, n, mean in counter_stats(a.db):
+            print("%-60s %-12s %8d %16.1f" % (k[:60], ctr, n, mean))
+    else:
+        print("%-60s %6s %12s %12s %12s %12s %14s" % ("kernel", "calls", "avg_us", "median_us", "min_us", "max_us",
+                                                       "total_us"))
+        for k, n, avg, med, mn, mx, tot in kernel_stats(a.db):
+            print("%-60s %6d %12.1f %12.1f %12.1f %12.1f %14.1f" % (k[:60], n, avg, med, mn, mx, tot))
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -26,7 +26,7 @@ def lib():
 
 def test_exports_every_declared_symbol(lib):
     names = _declared()
-    assert len(names) == 10, names
+    assert len(names) == 12, names
     for n in names:
         assert hasattr(lib, n), n
     from paper_2010_13359_amd import dqgan
@@ -77,3 +77,5 @@ def test_null_arguments(lib):
     assert lib.dqgan_unpack(None, ctypes.byref(w), None, None) == dqgan.EINVAL
     assert lib.dqgan_pack(None, None, None, ctypes.byref(w), None) == dqgan.EINVAL
     assert lib.dqgan_wire_bytes(None, None, None, None, None, None) == dqgan.EINVAL
+    assert lib.dqgan_step_scales(None, 0.1, None, None, ctypes.byref(w), None) == dqgan.EINVAL
+    assert lib.dqgan_step_apply(None, 0.1, 0, None, None, None, None, ctypes.byref(w), None, None) == dqgan.EINVAL
