@@ -30,9 +30,18 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "GB/s of gradient processed per fused compress+EF+aggregate+OMD step; % HBM peak"
 
 
-def source_hash():
+KERNEL_SOURCES = {
+    "dense": ("dense.hip", "device.hpp", "plan.hpp"),
+    "topk": ("topk.hip", "device.hpp", "plan.hpp"),
+}
+
+
+def source_hash(group="dense"):
+    """Hash of the sources a kernel family is built from (the counters in
+    profiles/traffic.json are valid only for the sources they were taken on)."""
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_2010_13359_amd", "csrc", "*"))):
+    for name in KERNEL_SOURCES[group]:
+        p = os.path.join(ROOT, "paper_2010_13359_amd", "csrc", name)
         with open(p, "rb") as f:
             h.update(os.path.basename(p).encode())
             h.update(f.read())
@@ -63,7 +72,7 @@ def workload_label(w):
     return "C%d %s: d=%d, M=%d workers, %s, %d segments, eta=%g" % (w.index, w.name, w.d, w.M, comp, w.n_seg, w.eta)
 
 
-def traffic_record(kernel_key):
+def traffic_record(kernel_key, group):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     if it was taken on the current kernel sources; else None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -74,7 +83,7 @@ def traffic_record(kernel_key):
             rec = json.load(f).get(kernel_key)
     except (ValueError, OSError):
         return None
-    if not rec or rec.get("source_hash") != source_hash():
+    if not rec or rec.get("source_hash") != source_hash(group):
         return None
     return rec.get("bytes_per_launch")
 
@@ -182,7 +191,7 @@ def main():
     achieved = b_alg / (t_apply * 1e-3) / 1e9
     step_ach = b_alg / (ms_step * 1e-3) / 1e9
     kernel_key = "apply_C%d" % w.index
-    traffic = traffic_record(kernel_key)
+    traffic = traffic_record(kernel_key, "topk" if w.kind == "topk" else "dense")
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",

@@ -328,6 +328,116 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
     }
 }
 
+// The fused step with the rows split across the NG waves of a workgroup:
+// all waves cover the same 64 quads, wave g owns rows g*R .. g*R+R-1 (rows
+// at or beyond M are skipped) and keeps only their p-hat and extrapolation
+// operands in registers.  The server sum runs in ascending worker order as a
+// chain through LDS: wave g adds its rows to the partial sum of waves
+// 0..g-1, so the result is the same sequential binary32 sum as in the
+// one-lane-per-quad kernel.  Few registers per lane leave room for many
+// waves per SIMD, which keeps enough loads in flight to stream from HBM.
+template <int KIND, int LB, int R, int NG>
+__global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict__ G, float *__restrict__ E,
+                                                         float *__restrict__ W, float *__restrict__ WX,
+                                                         float *__restrict__ Qhat, uint32_t *__restrict__ sign_plane,
+                                                         uint32_t *__restrict__ level_plane, float *__restrict__ val,
+                                                         const float2 *__restrict__ consts,
+                                                         const int64_t *__restrict__ off,
+                                                         const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
+    __shared__ f32x4 chain[64];
+    const int lane = threadIdx.x & 63;
+    const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
+    const int M = a.M;
+    const int last_g = (M - 1) / R;  // the wave that finishes the sum
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * 64 + lane;
+    const int64_t i0 = 4 * q;
+    int js[4];
+    lookup_segments(off, tile_seg, i0, a.d, js);
+    // One segment for the whole wave (the common case): its constants are
+    // fetched with one scalar load per row.
+    const int j_first = __builtin_amdgcn_readfirstlane(js[0]);
+    const bool one_seg = __ballot(js[0] != j_first || js[3] != j_first) == 0;
+    f32x4 ph[R], xs[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int m = g * R + r;
+        if (m < M) {
+            const int64_t rb = static_cast<int64_t>(m) * a.ld;
+            const f32x4 gv = ld_stream(G + rb + i0);
+            const f32x4 ev = ld_stream(E + rb + i0);
+            const float2 *crow = consts + static_cast<int64_t>(m) * a.n_seg;
+            QuadCodes cq;
+            if (one_seg) {
+                const float2 cu = crow[j_first];
+                const float2 c4[1] = {cu};
+                const int z[4] = {0, 0, 0, 0};
+                cq = encode_quad<KIND>(gv, ev, a.eta, i0, a.d, m, z, c4, a.s, a.k0, a.k1, a.t);
+            } else {
+                cq = encode_quad<KIND>(gv, ev, a.eta, i0, a.d, m, js, crow, a.s, a.k0, a.k1, a.t);
+            }
+            st_stream(E + rb + i0, cq.enew);
+            store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq);
+            ph[r] = cq.phat;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) set_elem(xs[r], c, add_rn(elem(cq.eg, c), elem(cq.enew, c)));
+        }
+    }
+#pragma unroll
+    for (int phase = 0; phase < NG; ++phase) {
+        if (phase <= last_g) {
+            if (g == phase) {
+                f32x4 acc;
+                if (phase == 0) {
+                    acc = ph[0];
+                } else {
+                    acc = chain[lane];
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) set_elem(acc, c, add_rn(elem(acc, c), elem(ph[0], c)));
+                }
+#pragma unroll
+                for (int r = 1; r < R; ++r) {
+                    if (g * R + r < M) {
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) set_elem(acc, c, add_rn(elem(acc, c), elem(ph[r], c)));
+                    }
+                }
+                if (phase < last_g) {
+                    chain[lane] = acc;
+                } else {
+                    f32x4 qh;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const float sacc = elem(acc, c);
+                        set_elem(qh, c, invM > 0.0f ? mul_rn(sacc, invM)
+                                                    : static_cast<float>(static_cast<double>(sacc) /
+                                                                         static_cast<double>(M)));
+                    }
+                    const f32x4 w = ld4(W + i0);
+                    f32x4 wt;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) set_elem(wt, c, sub_rn(elem(w, c), elem(qh, c)));
+                    st4(W + i0, wt);
+                    if (Qhat) st4(Qhat + i0, qh);
+                    chain[lane] = wt;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    const f32x4 wt = chain[lane];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const int m = g * R + r;
+        if (m < M) {
+            const int64_t rb = static_cast<int64_t>(m) * a.ld;
+            f32x4 wx;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) set_elem(wx, c, (i0 + c < a.d) ? sub_rn(elem(wt, c), elem(xs[r], c)) : 0.0f);
+            st_stream(WX + rb + i0, wx);
+        }
+    }
+}
+
 // Decode one quad of one row's message to p-hat.
 template <int KIND, int LB>
 __device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_row, const uint32_t *__restrict__ level_row,
@@ -493,18 +603,28 @@ hipError_t fused_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
     return hipGetLastError();
 }
 
+template <int KIND, int LB, int R, int NG>
+hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
+                        const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    hipLaunchKernelGGL((k_fused_split<KIND, LB, R, NG>), dim3(static_cast<unsigned>(P.n_tiles * 4)), dim3(64 * NG), 0,
+                       st, G, E, W, WX, Qhat, w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a,
+                       inv_m(P.desc.M));
+    return hipGetLastError();
+}
+
+// Launch shape of the fused step: up to 16 waves per workgroup, each owning
+// R = ceil(M / 16) rows (measured on C3, M = 32: 16 waves x 2 rows beats 8 x 4
+// and 4 x 8); larger M uses the one-lane-per-quad kernel.
 template <int KIND, int LB>
 hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                       const dqgan_wire &w, float *Qhat, hipStream_t st) {
-    switch (P.desc.M) {
-        case 1: return fused_launch<KIND, LB, 1>(P, a, G, E, W, WX, w, Qhat, st);
-        case 2: return fused_launch<KIND, LB, 2>(P, a, G, E, W, WX, w, Qhat, st);
-        case 4: return fused_launch<KIND, LB, 4>(P, a, G, E, W, WX, w, Qhat, st);
-        case 8: return fused_launch<KIND, LB, 8>(P, a, G, E, W, WX, w, Qhat, st);
-        case 16: return fused_launch<KIND, LB, 16>(P, a, G, E, W, WX, w, Qhat, st);
-        case 32: return fused_launch<KIND, LB, 32>(P, a, G, E, W, WX, w, Qhat, st);
-        default: return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
-    }
+    const int M = P.desc.M;
+    if (M <= 4) return split_launch<KIND, LB, 1, 4>(P, a, G, E, W, WX, w, Qhat, st);
+    if (M <= 8) return split_launch<KIND, LB, 1, 8>(P, a, G, E, W, WX, w, Qhat, st);
+    if (M <= 16) return split_launch<KIND, LB, 1, 16>(P, a, G, E, W, WX, w, Qhat, st);
+    if (M <= 32) return split_launch<KIND, LB, 2, 16>(P, a, G, E, W, WX, w, Qhat, st);
+    if (M <= 64) return split_launch<KIND, LB, 4, 16>(P, a, G, E, W, WX, w, Qhat, st);
+    return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
 }
 
 }  // namespace

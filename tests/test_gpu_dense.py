@@ -34,6 +34,10 @@ CASES = {
     "qsgd255_linf_m16": lambda: custom(d=40000, M=16, kind="qsgd", levels=255, norm="linf",
                                        seg_offsets=[0, 100, 40000], eta=1e-2, seed=10),
     "qsgd255_m64_generic": lambda: custom(d=2048, M=64, kind="qsgd", levels=255, eta=1e-2, seed=11),
+    "qsgd15_m17_masked": lambda: custom(d=6000, M=17, kind="qsgd", levels=15, seg_offsets=[0, 2999, 6000],
+                                        eta=1e-2, seed=16),
+    "sign_m33_masked": lambda: custom(d=4100, M=33, kind="sign", seg_offsets=[0, 64, 4100], eta=1e-2, seed=17),
+    "qsgd15_m65_one_lane": lambda: custom(d=3000, M=65, kind="qsgd", levels=15, eta=1e-2, seed=18),
     "identity_m2": lambda: custom(d=4097, M=2, kind="identity", eta=1e-2, seed=12),
     "identity_m1": lambda: custom(d=1500, M=1, kind="identity", eta=1e-2, seed=13),
 }
