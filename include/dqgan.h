@@ -88,7 +88,8 @@ typedef struct {
                                      TOPK, IDENTITY: DQGAN_NORM_NONE               */
     int32_t levels;               /* QSGD s: 255 (8-bit level field) or 15 (4-bit) */
     int32_t reserved;             /* must be 0                                      */
-    int64_t k;                    /* TOPK: 1 <= k <= d, d < 2^32                    */
+    int64_t k;                    /* TOPK: 1 <= k <= d, d < 2^32, M <= 64
+                                     (larger M: DQGAN_EUNSUPPORTED)                 */
     uint64_t seed;                /* QSGD: key of the Philox4x32-10 generator       */
 } dqgan_desc;
 

@@ -19,7 +19,7 @@ namespace dq {
 
 namespace {
 
-enum { kSign = DQGAN_SIGN, kQsgd = DQGAN_QSGD, kIdentity = DQGAN_IDENTITY };
+enum { kSign = DQGAN_SIGN, kQsgd = DQGAN_QSGD, kTopk = DQGAN_TOPK, kIdentity = DQGAN_IDENTITY };
 
 // ---------------------------------------------------------------------------
 // Pass 1: segment statistics.
@@ -190,6 +190,59 @@ __device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, f
     return o;
 }
 
+// Top-k (Theorem 1): p-hat = p on the selected elements, 0 elsewhere;
+// sign_nib carries the selection mask of the quad.
+__device__ __forceinline__ QuadCodes encode_quad_topk(const f32x4 g, const f32x4 e, float eta, int64_t i0, int64_t d,
+                                                      uint32_t T, uint32_t I) {
+    QuadCodes o;
+    o.sign_nib = 0u;
+    o.levels = 0u;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const float gc = elem(g, c), ec = elem(e, c);
+        const float egc = mul_rn(eta, gc);
+        const float p = add_rn(egc, ec);
+        float q = 0.0f, en = ec, egk = 0.0f;
+        const int64_t i = i0 + c;
+        if (i < d) {
+            egk = egc;
+            const uint32_t key = __float_as_uint(p) & 0x7FFFFFFFu;
+            const bool sel = key > T || (key == T && static_cast<uint32_t>(i) <= I);
+            q = sel ? p : 0.0f;
+            en = sub_rn(p, q);
+            o.sign_nib |= (sel ? 1u : 0u) << c;
+        }
+        set_elem(o.eg, c, egk);
+        set_elem(o.phat, c, q);
+        set_elem(o.enew, c, en);
+    }
+    return o;
+}
+
+// Ordered compaction of one row's selected elements of a 256-element tile
+// (the wave's 64 quads, element 4*lane + c): the position is the tile's
+// offset plus the number of selected elements before it in the tile.
+__device__ __forceinline__ void store_topk(float *__restrict__ val_row, uint32_t *__restrict__ idx_row, int64_t k,
+                                           uint32_t tile_base, int64_t i0, const QuadCodes &cq) {
+    const uint32_t mask = cq.sign_nib;
+    const int lane = threadIdx.x & 63;
+    const uint64_t below = (uint64_t(1) << lane) - 1;
+    uint32_t pre = 0;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) pre += __popcll(__ballot((mask >> c) & 1u) & below);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        if ((mask >> c) & 1u) {
+            const int64_t pos = static_cast<int64_t>(tile_base) + pre;
+            if (pos < k) {
+                val_row[pos] = elem(cq.phat, c);
+                idx_row[pos] = static_cast<uint32_t>(i0 + c);
+            }
+            ++pre;
+        }
+    }
+}
+
 __device__ __forceinline__ void lookup_segments(const int64_t *__restrict__ off, const int32_t *__restrict__ tile_seg,
                                                 int64_t i0, int64_t d, int js[4]) {
     const int64_t last = d - 1;
@@ -343,7 +396,8 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
                                                          uint32_t *__restrict__ level_plane, float *__restrict__ val,
                                                          const float2 *__restrict__ consts,
                                                          const int64_t *__restrict__ off,
-                                                         const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
+                                                         const int32_t *__restrict__ tile_seg, RowArgs a, float invM,
+                                                         TopkArgs ta) {
     __shared__ f32x4 chain[64];
     const int lane = threadIdx.x & 63;
     const int g = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x >> 6));
@@ -367,7 +421,10 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
             const f32x4 ev = ld_stream(E + rb + i0);
             const float2 *crow = consts + static_cast<int64_t>(m) * a.n_seg;
             QuadCodes cq;
-            if (one_seg) {
+            if constexpr (KIND == kTopk) {
+                const TopkRow *rw = ta.rows + m;
+                cq = encode_quad_topk(gv, ev, a.eta, i0, a.d, rw->T, rw->I);
+            } else if (one_seg) {
                 const float2 cu = crow[j_first];
                 const float2 c4[1] = {cu};
                 const int z[4] = {0, 0, 0, 0};
@@ -376,7 +433,12 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
                 cq = encode_quad<KIND>(gv, ev, a.eta, i0, a.d, m, js, crow, a.s, a.k0, a.k1, a.t);
             }
             st_stream(E + rb + i0, cq.enew);
-            store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq);
+            if constexpr (KIND == kTopk) {
+                store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + blockIdx.x], i0, cq);
+            } else {
+                store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q,
+                                        cq);
+            }
             ph[r] = cq.phat;
 #pragma unroll
             for (int c = 0; c < 4; ++c) set_elem(xs[r], c, add_rn(elem(cq.eg, c), elem(cq.enew, c)));
@@ -575,6 +637,21 @@ __global__ __launch_bounds__(kBlock) void k_pack(const uint16_t *__restrict__ co
         store_message<kQsgd, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, nullptr, q, cq);
 }
 
+// Top-k worker side only (dqgan_compress_ef): one wave per (tile, worker).
+__global__ __launch_bounds__(64) void k_topk_encode_rows(const float *__restrict__ G, float *__restrict__ E,
+                                                         float *__restrict__ val, RowArgs a, TopkArgs ta) {
+    const int m = blockIdx.y;
+    const int64_t q = static_cast<int64_t>(blockIdx.x) * 64 + threadIdx.x;
+    const int64_t i0 = 4 * q;
+    const int64_t rb = static_cast<int64_t>(m) * a.ld;
+    const TopkRow *rw = ta.rows + m;
+    const f32x4 g = ld_stream(G + rb + i0);
+    const f32x4 e = ld_stream(E + rb + i0);
+    const QuadCodes cq = encode_quad_topk(g, e, a.eta, i0, a.d, rw->T, rw->I);
+    st_stream(E + rb + i0, cq.enew);
+    store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + blockIdx.x], i0, cq);
+}
+
 RowArgs row_args(const dqgan_plan_s &P, float eta, uint32_t t) {
     RowArgs a;
     a.eta = eta;
@@ -606,9 +683,17 @@ hipError_t fused_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
 template <int KIND, int LB, int R, int NG>
 hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                         const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    TopkArgs ta{};
+    if (KIND == kTopk) {
+        ta.rows = P.topk.rows;
+        ta.tile_off = P.topk.tile_off;
+        ta.n_tiles = P.topk.n_tiles;
+        ta.k = P.desc.k;
+        ta.idx = w.idx;
+    }
     hipLaunchKernelGGL((k_fused_split<KIND, LB, R, NG>), dim3(static_cast<unsigned>(P.n_tiles * 4)), dim3(64 * NG), 0,
                        st, G, E, W, WX, Qhat, w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a,
-                       inv_m(P.desc.M));
+                       inv_m(P.desc.M), ta);
     return hipGetLastError();
 }
 
@@ -624,7 +709,11 @@ hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, f
     if (M <= 16) return split_launch<KIND, LB, 1, 16>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 32) return split_launch<KIND, LB, 2, 16>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 64) return split_launch<KIND, LB, 4, 16>(P, a, G, E, W, WX, w, Qhat, st);
-    return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
+    if constexpr (KIND == kTopk) {
+        return hipErrorNotSupported;  // top-k plans are limited to M <= 64
+    } else {
+        return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
+    }
 }
 
 }  // namespace
@@ -743,6 +832,21 @@ hipError_t launch_aggregate_dense(const dqgan_plan_s &P, const dqgan_wire &w, fl
     else
         hipLaunchKernelGGL((k_aggregate<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
                            P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_apply(const dqgan_plan_s &P, float eta, const float *G, float *E, float *W, float *WX,
+                             const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    const RowArgs a = row_args(P, eta, 0);
+    return fused_by_m<kTopk, 0>(P, a, G, E, W, WX, w, Qhat, st);
+}
+
+hipError_t launch_topk_encode_rows(const dqgan_plan_s &P, float eta, const float *G, float *E, const dqgan_wire &w,
+                                   hipStream_t st) {
+    const RowArgs a = row_args(P, eta, 0);
+    TopkArgs ta{P.topk.rows, P.topk.tile_off, P.topk.n_tiles, P.desc.k, w.idx};
+    hipLaunchKernelGGL(k_topk_encode_rows, dim3(static_cast<unsigned>(P.topk.n_tiles), static_cast<unsigned>(P.desc.M)),
+                       dim3(64), 0, st, G, E, w.val, a, ta);
     return hipGetLastError();
 }
 

@@ -19,13 +19,45 @@ struct Piece {
 };
 constexpr int64_t kPieceElems = 16384;
 
+// Per-worker selection state of the top-k compressor.  Keys are the binary32
+// bit patterns of |p| (monotone in |p|).  Element i is selected iff
+// key > T, or key == T and i <= I.
+struct TopkRow {
+    uint32_t lo, hi;     // candidate band [lo, hi] of keys, from the sample
+    uint32_t n_cand;     // candidates appended by the full pass (may exceed the capacity)
+    uint32_t fallback;   // 1: the band missed the k-th key; the full-row search decides
+    uint32_t T, I;       // the selection
+    uint32_t rank;       // full-row search: rank still to place
+    uint32_t kprefix;    // full-row search: key bits decided so far
+    uint32_t iprefix;    // full-row search: ~index bits decided so far
+    uint32_t done;       // full-row search finished early (all ties taken)
+    uint32_t total;      // selected count found by the tile scan (equals k)
+    uint32_t pad[5];
+};
+
+constexpr int kTopkTile = 256;            // elements per counting tile (one wave of quads)
+constexpr int kSampleBins = 32768;        // sample histogram: key >> 16 (keys < 2^31)
+constexpr int64_t kSampleStride = 65536;  // one 256-element chunk sampled per 65536 elements
+
 // Top-k workspace (one set per plan).
 struct TopkScratch {
-    uint32_t *hist = nullptr;       // [M][kHistBins] counts of the current digit
-    uint32_t *state = nullptr;      // [M][kTopkState] selection state per row
-    uint32_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per tile
+    TopkRow *rows = nullptr;        // [M]
+    uint32_t *hist = nullptr;       // [M][kSampleBins] sample histogram; [M][2048] digit histogram
+    uint2 *cand = nullptr;          // [M][cap] (key, index) candidates
+    int64_t cap = 0;
+    uint32_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per 256-element tile
     uint32_t *tile_off = nullptr;   // [M][n_tiles] exclusive prefix of tile_cnt
     int64_t n_tiles = 0;
+    int64_t n_chunks = 0;           // sampled chunks per row
+    uint32_t n_samples = 0;         // sampled elements per row
+};
+
+struct TopkArgs {
+    const TopkRow *rows;
+    const uint32_t *tile_off;
+    int64_t n_tiles;
+    int64_t k;
+    uint32_t *idx;
 };
 
 }  // namespace dq
@@ -72,6 +104,8 @@ hipError_t launch_topk_compress(const dqgan_plan_s &P, float eta, const float *G
 hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, const float *E, hipStream_t st);
 hipError_t launch_topk_apply(const dqgan_plan_s &P, float eta, const float *G, float *E, float *W, float *WX,
                              const dqgan_wire &w, float *Qhat, hipStream_t st);
+hipError_t launch_topk_encode_rows(const dqgan_plan_s &P, float eta, const float *G, float *E, const dqgan_wire &w,
+                                   hipStream_t st);
 hipError_t launch_topk_unpack(const dqgan_plan_s &P, const dqgan_wire &w, float *Phat, hipStream_t st);
 hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st);
 

@@ -1,26 +1,569 @@
-// Top-k compressor (Theorem 1 of arXiv:2010.13359): placeholder launchers,
-// replaced by the radix-select path.
+// Top-k compressor (Theorem 1 of arXiv:2010.13359: keep the k entries of
+// largest magnitude; ties go to the lower index) -- the selection pass.
+//
+// Keys are the binary32 bit patterns of |p| (p = fl(fl(eta g) + e)), which
+// order like |p|.  The selection of a row is the k largest composite keys
+// (key, ~index): element i is selected iff key > T, or key == T and i <= I.
+//
+// Per row, with one full read of g and e:
+//  1. sample: one 256-element chunk per 65536 elements, histogram of key>>16;
+//  2. band: the sample ranks k/d * s -+ 8 sigma bracket the k-th key in a
+//     band [lo, hi];
+//  3. full pass: per 256-element tile the number of keys above hi, and every
+//     in-band (key, index) appended to a candidate list;
+//  4. exact radix select of the remaining rank among the candidates (six
+//     digits of the composite key) gives T and I;
+//  5. the selected candidates are added to their tiles' counts.
+// If the band missed the k-th key (or the candidates overflow), the row falls
+// back to a full-row radix select over the same six digits (one read of the
+// row per digit) and a recount.  Finally an exclusive scan of the tile
+// counts gives each tile's first output position, which the fused apply
+// pass uses to write (value, index) in ascending index order.
+#include "device.hpp"
 #include "plan.hpp"
 
 namespace dq {
 
-hipError_t topk_alloc(dqgan_plan_s &) { return hipSuccess; }
-void topk_free(dqgan_plan_s &) {}
-hipError_t launch_topk_compress(const dqgan_plan_s &, float, const float *, float *, const dqgan_wire &, hipStream_t) {
-    return hipErrorNotSupported;
+namespace {
+
+constexpr int kDigitBins = 2048;
+constexpr int kFbBlocks = 128;  // workgroups per row of the full-row search
+
+__device__ __forceinline__ uint32_t key_of(float g, float e, float eta) {
+    const float p = add_rn(mul_rn(eta, g), e);
+    return __float_as_uint(p) & 0x7FFFFFFFu;
 }
-hipError_t launch_topk_select(const dqgan_plan_s &, float, const float *, const float *, hipStream_t) {
-    return hipErrorNotSupported;
+
+__global__ __launch_bounds__(kBlock) void k_fill_u32(uint32_t *__restrict__ p, int64_t n, uint32_t v) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * kBlock)
+        p[i] = v;
 }
-hipError_t launch_topk_apply(const dqgan_plan_s &, float, const float *, float *, float *, float *, const dqgan_wire &,
-                             float *, hipStream_t) {
-    return hipErrorNotSupported;
+
+__global__ __launch_bounds__(kBlock) void k_fill_f32(float *__restrict__ p, int64_t n) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * kBlock)
+        p[i] = 0.0f;
 }
-hipError_t launch_topk_unpack(const dqgan_plan_s &, const dqgan_wire &, float *, hipStream_t) {
-    return hipErrorNotSupported;
+
+// Digit of a composite key for pass 0..5 and the filter of elements still in
+// play (those whose decided digits equal the prefixes found so far).
+__device__ __forceinline__ uint32_t digit_of(int pass, uint32_t key, uint32_t ni) {
+    switch (pass) {
+        case 0: return key >> 20;
+        case 1: return (key >> 9) & 0x7FFu;
+        case 2: return key & 0x1FFu;
+        case 3: return ni >> 21;
+        case 4: return (ni >> 10) & 0x7FFu;
+        default: return ni & 0x3FFu;
+    }
 }
-hipError_t launch_topk_aggregate(const dqgan_plan_s &, const dqgan_wire &, float *, hipStream_t) {
-    return hipErrorNotSupported;
+__device__ __forceinline__ bool in_play(int pass, uint32_t key, uint32_t ni, uint32_t kp, uint32_t ip) {
+    switch (pass) {
+        case 0: return true;
+        case 1: return (key >> 20) == (kp >> 20);
+        case 2: return (key >> 9) == (kp >> 9);
+        case 3: return key == kp;
+        case 4: return key == kp && (ni >> 21) == (ip >> 21);
+        default: return key == kp && (ni >> 10) == (ip >> 10);
+    }
+}
+__host__ __device__ __forceinline__ int bins_of(int pass) { return pass == 2 ? 512 : pass == 5 ? 1024 : 2048; }
+__device__ __forceinline__ void add_prefix(int pass, uint32_t bin, uint32_t &kp, uint32_t &ip) {
+    switch (pass) {
+        case 0: kp |= bin << 20; break;
+        case 1: kp |= bin << 9; break;
+        case 2: kp |= bin; break;
+        case 3: ip |= bin << 21; break;
+        case 4: ip |= bin << 10; break;
+        default: ip |= bin; break;
+    }
+}
+
+// One wave finds, in a histogram of nb bins, the bin holding the rank-th
+// largest item (rank >= 1) and the count of items in higher bins.  Returns
+// false if the histogram holds fewer than rank items.
+__device__ bool wave_find_desc(const uint32_t *h, int nb, uint32_t rank, uint32_t &bin, uint32_t &above) {
+    const int lane = threadIdx.x & 63;
+    const int per = (nb + 63) / 64;
+    uint32_t s = 0;
+    for (int j = 0; j < per; ++j) {
+        const int b = nb - 1 - (lane * per + j);
+        if (b >= 0) s += h[b];
+    }
+    uint32_t incl = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t v = __shfl_up(incl, o);
+        if (lane >= o) incl += v;
+    }
+    const uint32_t excl = incl - s;
+    const uint64_t hit = __ballot(excl < rank && rank <= incl);
+    if (!hit) return false;
+    const int L = __ffsll(static_cast<unsigned long long>(hit)) - 1;
+    uint32_t rb = 0, ra = 0;
+    if (lane == L) {
+        uint32_t acc = excl;
+        for (int j = 0; j < per; ++j) {
+            const int b = nb - 1 - (lane * per + j);
+            if (b < 0) break;
+            if (acc + h[b] >= rank) {
+                rb = static_cast<uint32_t>(b);
+                ra = acc;
+                break;
+            }
+            acc += h[b];
+        }
+    }
+    bin = __shfl(rb, L);
+    above = __shfl(ra, L);
+    return true;
+}
+
+// 1. Sample histogram of key >> 16 (one 256-element chunk per 65536 elements).
+__global__ __launch_bounds__(kBlock) void k_topk_sample(const float *__restrict__ G, const float *__restrict__ E,
+                                                        float eta, int64_t d, int64_t ld, int64_t n_chunks,
+                                                        uint32_t *__restrict__ hist) {
+    __shared__ uint32_t h[kSampleBins];
+    const int m = blockIdx.y;
+    for (int b = threadIdx.x; b < kSampleBins; b += kBlock) h[b] = 0;
+    __syncthreads();
+    const float *g = G + static_cast<int64_t>(m) * ld;
+    const float *e = E + static_cast<int64_t>(m) * ld;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + wave; c < n_chunks;
+         c += static_cast<int64_t>(gridDim.x) * 4) {
+        const int64_t i0 = c * kSampleStride + 4 * lane;
+        if (i0 < d) {
+            const f32x4 gv = ld4(g + i0), ev = ld4(e + i0);
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                if (i0 + k < d) atomicAdd(&h[key_of(elem(gv, k), elem(ev, k), eta) >> 16], 1u);
+        }
+    }
+    __syncthreads();
+    uint32_t *hm = hist + static_cast<int64_t>(m) * kSampleBins;
+    for (int b = threadIdx.x; b < kSampleBins; b += kBlock)
+        if (h[b]) atomicAdd(&hm[b], h[b]);
+}
+
+// 2. Candidate band of each row from its sample histogram.
+__global__ __launch_bounds__(64) void k_topk_band(const uint32_t *__restrict__ hist, TopkRow *__restrict__ rows,
+                                                  uint32_t n_samples, int64_t d, int64_t k) {
+    const int m = blockIdx.x;
+    const uint32_t *h = hist + static_cast<int64_t>(m) * kSampleBins;
+    const double f = static_cast<double>(k) / static_cast<double>(d);
+    const double s = static_cast<double>(n_samples);
+    const double mean = f * s;
+    const double sd = sqrt(s * f * (1.0 - f)) + 1.0;
+    const double z = 8.0;
+    uint32_t hi = 0x7FFFFFFFu, lo = 0u;
+    const double a = floor(mean - z * sd);
+    uint32_t bin, above;
+    if (a >= 1.0 && wave_find_desc(h, kSampleBins, static_cast<uint32_t>(a) + 1u, bin, above))
+        hi = ((bin + 1u) << 16) - 1u;
+    const double c = ceil(mean + z * sd);
+    if (c <= s && wave_find_desc(h, kSampleBins, static_cast<uint32_t>(c), bin, above)) lo = bin << 16;
+    if (lo > hi) lo = 0u;
+    if (threadIdx.x == 0) {
+        TopkRow r{};
+        r.lo = lo;
+        r.hi = hi;
+        rows[m] = r;
+    }
+}
+
+// 3. Full pass: per tile the count of keys above the band, and the in-band
+// candidates appended to the row's list.  A workgroup covers 16 tiles of one
+// row (4 waves x 4 tiles) and appends its candidates with one atomic.
+__global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
+                                                      float eta, int64_t d, int64_t ld, int64_t n_tiles,
+                                                      TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
+                                                      uint2 *__restrict__ cand, int64_t cap) {
+    __shared__ uint2 buf[16 * kTopkTile];
+    __shared__ uint32_t nbuf, base;
+    const int m = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t lo = rows[m].lo, hi = rows[m].hi;
+    const float *g = G + static_cast<int64_t>(m) * ld;
+    const float *e = E + static_cast<int64_t>(m) * ld;
+    if (threadIdx.x == 0) nbuf = 0;
+    __syncthreads();
+    const uint64_t below = (uint64_t(1) << lane) - 1;
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int64_t tile = static_cast<int64_t>(blockIdx.x) * 16 + it * 4 + wave;
+        if (tile < n_tiles) {
+            const int64_t i0 = tile * kTopkTile + 4 * lane;
+            const f32x4 gv = ld_stream(g + i0), ev = ld_stream(e + i0);
+            uint32_t keys[4];
+            uint32_t above_n = 0, cmask = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                keys[k] = key_of(elem(gv, k), elem(ev, k), eta);
+                const bool valid = i0 + k < d;
+                above_n += __popcll(__ballot(valid && keys[k] > hi));
+                cmask |= ((valid && keys[k] >= lo && keys[k] <= hi) ? 1u : 0u) << k;
+            }
+            if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
+            uint32_t pre = 0, tot = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const uint64_t b = __ballot((cmask >> k) & 1u);
+                pre += __popcll(b & below);
+                tot += __popcll(b);
+            }
+            if (tot) {
+                uint32_t wbase = 0;
+                if (lane == 0) wbase = atomicAdd(&nbuf, tot);
+                wbase = __shfl(wbase, 0);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    if ((cmask >> k) & 1u) {
+                        buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                        ++pre;
+                    }
+                }
+            }
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) base = nbuf ? atomicAdd(&rows[m].n_cand, nbuf) : 0u;
+    __syncthreads();
+    uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    for (uint32_t j = threadIdx.x; j < nbuf; j += kBlock) {
+        const int64_t pos = static_cast<int64_t>(base) + j;
+        if (pos < cap) crow[pos] = buf[j];
+    }
+}
+
+// 4. Exact selection among the candidates (one workgroup per row).  Rows
+// whose band missed are handed to the full-row search.
+__global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows, const uint32_t *__restrict__ tile_cnt,
+                                                      int64_t n_tiles, const uint2 *__restrict__ cand, int64_t cap,
+                                                      int64_t k, uint32_t *__restrict__ hist) {
+    __shared__ uint32_t h[kDigitBins];
+    __shared__ unsigned long long red[16];
+    __shared__ uint32_t res[3];
+    const int m = blockIdx.x;
+    const int tid = threadIdx.x;
+    unsigned long long s = 0;
+    for (int64_t t = tid; t < n_tiles; t += 1024) s += tile_cnt[static_cast<int64_t>(m) * n_tiles + t];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+    if ((tid & 63) == 0) red[tid >> 6] = s;
+    __syncthreads();
+    unsigned long long n_above = 0;
+    for (int w = 0; w < 16; ++w) n_above += red[w];
+    const uint32_t n_cand = rows[m].n_cand;
+    const bool ok = n_cand <= cap && n_above < static_cast<unsigned long long>(k) &&
+                    static_cast<unsigned long long>(k) - n_above <= n_cand;
+    if (!ok) {
+        if (tid == 0) {
+            rows[m].fallback = 1u;
+            rows[m].rank = static_cast<uint32_t>(k);
+            rows[m].kprefix = 0u;
+            rows[m].iprefix = 0u;
+            rows[m].done = 0u;
+        }
+        uint32_t *hm = hist + static_cast<int64_t>(m) * kDigitBins;
+        for (int b = tid; b < kDigitBins; b += 1024) hm[b] = 0u;
+        return;
+    }
+    uint32_t rank = static_cast<uint32_t>(static_cast<unsigned long long>(k) - n_above);
+    uint32_t kp = 0, ip = 0, I = 0xFFFFFFFFu;
+    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    for (int pass = 0; pass < 6; ++pass) {
+        const int nb = bins_of(pass);
+        for (int b = tid; b < nb; b += 1024) h[b] = 0u;
+        __syncthreads();
+        for (uint32_t j = tid; j < n_cand; j += 1024) {
+            const uint2 c = crow[j];
+            const uint32_t ni = ~c.y;
+            if (in_play(pass, c.x, ni, kp, ip)) atomicAdd(&h[digit_of(pass, c.x, ni)], 1u);
+        }
+        __syncthreads();
+        if (tid < 64) {
+            uint32_t bin = 0, above = 0;
+            wave_find_desc(h, nb, rank, bin, above);
+            if (tid == 0) {
+                res[0] = bin;
+                res[1] = above;
+                res[2] = h[bin];
+            }
+        }
+        __syncthreads();
+        const uint32_t bin = res[0];
+        rank -= res[1];
+        add_prefix(pass, bin, kp, ip);
+        const uint32_t n_bin = res[2];
+        __syncthreads();
+        if (pass == 2 && rank == n_bin) break;  // every tie at T is taken
+        if (pass == 5) I = ~ip;
+    }
+    if (tid == 0) {
+        rows[m].T = kp;
+        rows[m].I = I;
+    }
+}
+
+// 5. Add the selected candidates to their tiles' counts.
+__global__ __launch_bounds__(kBlock) void k_topk_count(const TopkRow *__restrict__ rows, const uint2 *__restrict__ cand,
+                                                       int64_t cap, uint32_t *__restrict__ tile_cnt, int64_t n_tiles) {
+    const int m = blockIdx.y;
+    const TopkRow r = rows[m];
+    if (r.fallback) return;
+    const uint32_t n = r.n_cand;
+    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n;
+         j += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const uint2 c = crow[j];
+        if (c.x > r.T || (c.x == r.T && c.y <= r.I))
+            atomicAdd(&tile_cnt[static_cast<int64_t>(m) * n_tiles + (c.y >> 8)], 1u);
+    }
+}
+
+// 6. Full-row search of a row whose band missed: histogram of one digit ...
+__global__ __launch_bounds__(kBlock) void k_topk_fb_hist(int pass, const float *__restrict__ G,
+                                                         const float *__restrict__ E, float eta, int64_t d, int64_t ld,
+                                                         const TopkRow *__restrict__ rows,
+                                                         uint32_t *__restrict__ hist) {
+    __shared__ uint32_t h[kDigitBins];
+    const int m = blockIdx.y;
+    const TopkRow r = rows[m];
+    if (!r.fallback || r.done) return;
+    const int nb = bins_of(pass);
+    for (int b = threadIdx.x; b < nb; b += kBlock) h[b] = 0u;
+    __syncthreads();
+    const float *g = G + static_cast<int64_t>(m) * ld;
+    const float *e = E + static_cast<int64_t>(m) * ld;
+    const int64_t nq = (d + 3) / 4;
+    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nq;
+         q += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const f32x4 gv = ld4(g + 4 * q), ev = ld4(e + 4 * q);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int64_t i = 4 * q + k;
+            if (i < d) {
+                const uint32_t key = key_of(elem(gv, k), elem(ev, k), eta);
+                const uint32_t ni = ~static_cast<uint32_t>(i);
+                if (in_play(pass, key, ni, r.kprefix, r.iprefix)) atomicAdd(&h[digit_of(pass, key, ni)], 1u);
+            }
+        }
+    }
+    __syncthreads();
+    uint32_t *hm = hist + static_cast<int64_t>(m) * kDigitBins;
+    for (int b = threadIdx.x; b < nb; b += kBlock)
+        if (h[b]) atomicAdd(&hm[b], h[b]);
+}
+
+// ... then place the rank in it (one wave per row).
+__global__ __launch_bounds__(64) void k_topk_fb_digit(int pass, TopkRow *__restrict__ rows,
+                                                      uint32_t *__restrict__ hist) {
+    const int m = blockIdx.x;
+    TopkRow r = rows[m];
+    if (!r.fallback || r.done) return;
+    uint32_t *hm = hist + static_cast<int64_t>(m) * kDigitBins;
+    const int nb = bins_of(pass);
+    uint32_t bin = 0, above = 0;
+    wave_find_desc(hm, nb, r.rank, bin, above);
+    const uint32_t n_bin = hm[bin];
+    __syncthreads();
+    for (int b = threadIdx.x; b < kDigitBins; b += 64) hm[b] = 0u;
+    if (threadIdx.x == 0) {
+        r.rank -= above;
+        add_prefix(pass, bin, r.kprefix, r.iprefix);
+        if (pass == 2 && r.rank == n_bin) {
+            r.T = r.kprefix;
+            r.I = 0xFFFFFFFFu;
+            r.done = 1u;
+        } else if (pass == 2) {
+            r.T = r.kprefix;
+        } else if (pass == 5) {
+            r.I = ~r.iprefix;
+            r.done = 1u;
+        }
+        rows[m] = r;
+    }
+}
+
+// ... and count the selection per tile.
+__global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restrict__ G, const float *__restrict__ E,
+                                                            float eta, int64_t d, int64_t ld, int64_t n_tiles,
+                                                            const TopkRow *__restrict__ rows,
+                                                            uint32_t *__restrict__ tile_cnt) {
+    const int m = blockIdx.y;
+    const TopkRow r = rows[m];
+    if (!r.fallback) return;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float *g = G + static_cast<int64_t>(m) * ld;
+    const float *e = E + static_cast<int64_t>(m) * ld;
+    for (int64_t tile = static_cast<int64_t>(blockIdx.x) * 4 + wave; tile < n_tiles;
+         tile += static_cast<int64_t>(gridDim.x) * 4) {
+        const int64_t i0 = tile * kTopkTile + 4 * lane;
+        const f32x4 gv = ld4(g + i0), ev = ld4(e + i0);
+        uint32_t n = 0;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const int64_t i = i0 + k;
+            const uint32_t key = key_of(elem(gv, k), elem(ev, k), eta);
+            const bool sel = i < d && (key > r.T || (key == r.T && static_cast<uint32_t>(i) <= r.I));
+            n += __popcll(__ballot(sel));
+        }
+        if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = n;
+    }
+}
+
+// 7. Exclusive scan of the tile counts of each row (one workgroup per row).
+__global__ __launch_bounds__(1024) void k_topk_tile_scan(TopkRow *__restrict__ rows,
+                                                         const uint32_t *__restrict__ tile_cnt,
+                                                         uint32_t *__restrict__ tile_off, int64_t n_tiles) {
+    __shared__ uint32_t wsum[16];
+    const int m = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t per = (n_tiles + 1023) / 1024;
+    const int64_t a = static_cast<int64_t>(tid) * per;
+    const int64_t b = a + per < n_tiles ? a + per : n_tiles;
+    const uint32_t *cr = tile_cnt + static_cast<int64_t>(m) * n_tiles;
+    uint32_t *orow = tile_off + static_cast<int64_t>(m) * n_tiles;
+    uint32_t s = 0;
+    for (int64_t t = a; t < b; ++t) s += cr[t];
+    uint32_t incl = s;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t v = __shfl_up(incl, o);
+        if (lane >= o) incl += v;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t wbase = 0;
+    for (int w = 0; w < wave; ++w) wbase += wsum[w];
+    uint32_t run = wbase + incl - s;
+    for (int64_t t = a; t < b; ++t) {
+        orow[t] = run;
+        run += cr[t];
+    }
+    if (tid == 1023) rows[m].total = run;
+}
+
+// Server side: scatter the messages (unpack), or add them in worker order.
+__global__ __launch_bounds__(kBlock) void k_topk_scatter(const float *__restrict__ val, const uint32_t *__restrict__ idx,
+                                                         int64_t k, float *__restrict__ out, int64_t ld) {
+    const int m = blockIdx.y;
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < k;
+         j += static_cast<int64_t>(gridDim.x) * kBlock)
+        out[static_cast<int64_t>(m) * ld + idx[static_cast<int64_t>(m) * k + j]] = val[static_cast<int64_t>(m) * k + j];
+}
+
+__global__ __launch_bounds__(kBlock) void k_topk_scatter_add(const float *__restrict__ val,
+                                                             const uint32_t *__restrict__ idx, int64_t k,
+                                                             float *__restrict__ S) {
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < k;
+         j += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const uint32_t i = idx[j];
+        S[i] = add_rn(S[i], val[j]);
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void k_divide(float *__restrict__ S, int64_t n, int32_t M, float invM) {
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * kBlock)
+        S[i] = invM > 0.0f ? mul_rn(S[i], invM) : static_cast<float>(static_cast<double>(S[i]) / static_cast<double>(M));
+}
+
+unsigned grid_for(int64_t n, int64_t cap_blocks = 65536) {
+    int64_t b = (n + kBlock - 1) / kBlock;
+    if (b < 1) b = 1;
+    return static_cast<unsigned>(b < cap_blocks ? b : cap_blocks);
+}
+
+}  // namespace
+
+hipError_t topk_alloc(dqgan_plan_s &P) {
+    TopkScratch &S = P.topk;
+    const dqgan_desc &D = P.desc;
+    S.n_tiles = D.ld / kTopkTile;
+    S.n_chunks = (D.d + kSampleStride - 1) / kSampleStride;
+    int64_t ns = 0;
+    for (int64_t c = 0; c < S.n_chunks; ++c) {
+        const int64_t a = c * kSampleStride;
+        ns += (D.d - a < kTopkTile) ? D.d - a : kTopkTile;
+    }
+    S.n_samples = static_cast<uint32_t>(ns);
+    int64_t cap = D.k > 65536 ? D.k : 65536;
+    S.cap = cap < D.d ? cap : D.d;
+    const size_t M = static_cast<size_t>(D.M);
+    hipError_t e = hipMalloc(reinterpret_cast<void **>(&S.rows), M * sizeof(TopkRow));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.hist), M * kSampleBins * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.cand), M * static_cast<size_t>(S.cap) * sizeof(uint2));
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.tile_cnt), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.tile_off), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
+    return e;
+}
+
+void topk_free(dqgan_plan_s &P) {
+    TopkScratch &S = P.topk;
+    (void)hipFree(S.rows);
+    (void)hipFree(S.hist);
+    (void)hipFree(S.cand);
+    (void)hipFree(S.tile_cnt);
+    (void)hipFree(S.tile_off);
+    S = TopkScratch{};
+}
+
+hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, const float *E, hipStream_t st) {
+    const TopkScratch &S = P.topk;
+    const dqgan_desc &D = P.desc;
+    const unsigned M = static_cast<unsigned>(D.M);
+    const int64_t nh = static_cast<int64_t>(D.M) * kSampleBins;
+    hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(nh, 1024)), dim3(kBlock), 0, st, S.hist, nh, 0u);
+    const int64_t sb = (S.n_chunks + 3) / 4;
+    hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kBlock), 0, st, G, E, eta,
+                       D.d, D.ld, S.n_chunks, S.hist);
+    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(64), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
+    hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + 15) / 16), M), dim3(kBlock), 0, st, G, E,
+                       eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
+    hipLaunchKernelGGL(k_topk_select, dim3(M), dim3(1024), 0, st, S.rows, S.tile_cnt, S.n_tiles, S.cand, S.cap, D.k,
+                       S.hist);
+    hipLaunchKernelGGL(k_topk_count, dim3(64, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, S.tile_cnt, S.n_tiles);
+    for (int pass = 0; pass < 6; ++pass) {
+        hipLaunchKernelGGL(k_topk_fb_hist, dim3(kFbBlocks, M), dim3(kBlock), 0, st, pass, G, E, eta, D.d, D.ld, S.rows,
+                           S.hist);
+        hipLaunchKernelGGL(k_topk_fb_digit, dim3(M), dim3(64), 0, st, pass, S.rows, S.hist);
+    }
+    hipLaunchKernelGGL(k_topk_fb_recount, dim3(256, M), dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows,
+                       S.tile_cnt);
+    hipLaunchKernelGGL(k_topk_tile_scan, dim3(M), dim3(1024), 0, st, S.rows, S.tile_cnt, S.tile_off, S.n_tiles);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_compress(const dqgan_plan_s &P, float eta, const float *G, float *E, const dqgan_wire &w,
+                                hipStream_t st) {
+    hipError_t e = launch_topk_select(P, eta, G, E, st);
+    if (e != hipSuccess) return e;
+    return launch_topk_encode_rows(P, eta, G, E, w, st);
+}
+
+hipError_t launch_topk_unpack(const dqgan_plan_s &P, const dqgan_wire &w, float *Phat, hipStream_t st) {
+    const dqgan_desc &D = P.desc;
+    const int64_t n = static_cast<int64_t>(D.M) * D.ld;
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid_for(n)), dim3(kBlock), 0, st, Phat, n);
+    hipLaunchKernelGGL(k_topk_scatter, dim3(grid_for(D.k, 4096), static_cast<unsigned>(D.M)), dim3(kBlock), 0, st,
+                       w.val, w.idx, D.k, Phat, D.ld);
+    return hipGetLastError();
+}
+
+hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    const dqgan_desc &D = P.desc;
+    hipLaunchKernelGGL(k_fill_f32, dim3(grid_for(D.ld)), dim3(kBlock), 0, st, Qhat, D.ld);
+    for (int m = 0; m < D.M; ++m)
+        hipLaunchKernelGGL(k_topk_scatter_add, dim3(grid_for(D.k, 4096)), dim3(kBlock), 0, st,
+                           w.val + static_cast<int64_t>(m) * D.k, w.idx + static_cast<int64_t>(m) * D.k, D.k, Qhat);
+    const float im = (D.M & (D.M - 1)) == 0 ? 1.0f / static_cast<float>(D.M) : 0.0f;
+    hipLaunchKernelGGL(k_divide, dim3(grid_for(D.d)), dim3(kBlock), 0, st, Qhat, D.d, D.M, im);
+    return hipGetLastError();
 }
 
 }  // namespace dq

@@ -1,0 +1,142 @@
+"""GPU parity of the top-k compressor (Theorem 1; ties to the lower index)
+through the C ABI, against the oracle on the same inputs.  Indices and
+values of the message, residuals, the average and the OMD outputs must be
+identical.  Shapes cover the sampled-band path (Gaussian and Laplace data)
+and the full-row fallback (heavy ties, all-zero rows, k = d)."""
+import numpy as np
+import pytest
+
+from gpu_common import GpuState, assert_same, compare_step, inputs
+from synth.configs import custom
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(name):
+    if name == "m4_d5000_k50":
+        return custom(d=5000, M=4, kind="topk", k=50, eta=1e-2, seed=21), None
+    if name == "m8_d200000_k2000":
+        return custom(d=200000, M=8, kind="topk", k=2000, eta=1e-2, seed=22), None
+    if name == "m5_d3001_k7":
+        return custom(d=3001, M=5, kind="topk", k=7, eta=1e-2, seed=23), None
+    if name == "m64_d300000_k3000":
+        return custom(d=300000, M=64, kind="topk", k=3000, eta=1e-2, seed=24, law="laplace"), None
+    if name == "m3_d1_k1":
+        return custom(d=1, M=3, kind="topk", k=1, eta=1e-2, seed=25), None
+    if name == "m2_d4096_kd":
+        return custom(d=4096, M=2, kind="topk", k=4096, eta=1e-2, seed=26), None
+    if name == "m4_ties":
+        return custom(d=70000, M=4, kind="topk", k=7000, eta=1.0, seed=27), "ties"
+    if name == "m4_zero_rows":
+        # two all-zero rows: every key ties and the candidates overflow, so
+        # those rows take the full-row search
+        return custom(d=200000, M=4, kind="topk", k=2000, eta=1e-2, seed=28), "zeros"
+    if name == "m4_ties_big":
+        # 75% of the 300000 keys tie at |p| = 1: candidate overflow, full-row
+        # search including the index digits
+        return custom(d=300000, M=4, kind="topk", k=30000, eta=1.0, seed=31), "ties"
+    if name == "m2_hidden_cluster":
+        # 700 equal large values outside the sampled chunks: more than k keys
+        # lie above the band, so the full-row search decides
+        return custom(d=200000, M=2, kind="topk", k=500, eta=1e-2, seed=32), "cluster"
+    if name == "m16_d1000000_k10000":
+        return custom(d=1000000, M=16, kind="topk", k=10000, eta=1e-3, seed=29), None
+    raise KeyError(name)
+
+
+NAMES = ["m4_d5000_k50", "m8_d200000_k2000", "m5_d3001_k7", "m64_d300000_k3000", "m3_d1_k1", "m2_d4096_kd",
+         "m4_ties", "m4_ties_big", "m4_zero_rows", "m2_hidden_cluster", "m16_d1000000_k10000"]
+
+
+def _inputs(name):
+    w, special = _case(name)
+    G, E, W = inputs(w)
+    if special == "ties":
+        # gradients and residuals from a 4-value set: |p| has a handful of
+        # distinct values, so the k-th key is shared by thousands of elements
+        rng = np.random.default_rng(3)
+        G[:, :w.d] = rng.choice(np.array([0.5, -0.5, 1.0, -0.25], np.float32), size=(w.M, w.d))
+        E[:, :w.d] = 0.0
+    if special == "cluster":
+        G[:, 1000:1700] = 100.0
+        G[1, 1200:1300] = -100.0
+    if special == "zeros":
+        G[1, :] = 0.0
+        E[1, :] = 0.0
+        G[3, :] = -0.0
+        E[3, :] = 0.0
+    return w, G, E, W
+
+
+def _oracle(w, G, E, W):
+    from oracle import oracle as orc
+    return orc.step(w.as_dict(), np.float32(w.eta), 1, G, E.copy(), W.copy())
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_topk_fused_matches_oracle(name):
+    w, G, E, W = _inputs(name)
+    print("case", name, "d", w.d, "M", w.M, "k", w.k, flush=True)
+    s = GpuState(w, G, E, W)
+    s.fused(1)
+    gpu = s.host()
+    s.close()
+    ref = _oracle(w, G, E, W)
+    compare_step(w, gpu, ref)
+    assert np.all(np.diff(gpu["idx"].astype(np.int64), axis=1) > 0)
+
+
+@pytest.mark.parametrize("name", ["m4_d5000_k50", "m64_d300000_k3000", "m4_ties", "m4_zero_rows",
+                                  "m2_hidden_cluster"])
+def test_topk_unfused_equals_fused(name):
+    w, G, E, W = _inputs(name)
+    a = GpuState(w, G, E, W)
+    a.fused(1)
+    fa = a.host()
+    a.close()
+    b = GpuState(w, G, E, W)
+    b.unfused(1)
+    fb = b.host()
+    b.close()
+    compare_step(w, fa, fb)
+
+
+@pytest.mark.parametrize("name", ["m8_d200000_k2000", "m4_ties"])
+def test_topk_unpack(name):
+    import torch
+    w, G, E, W = _inputs(name)
+    s = GpuState(w, G, E, W)
+    s.dq.compress_ef(s.plan, w.eta, 1, s.G, s.E, None, s.wire)
+    Ph = torch.full((w.M, w.ld), float("nan"), dtype=torch.float32, device=s.G.device)
+    s.dq.unpack(s.plan, s.wire, Ph)
+    torch.cuda.synchronize()
+    got = Ph.cpu().numpy()
+    out = s.host()
+    s.close()
+    for m in range(w.M):
+        exp = np.zeros(w.ld, np.float32)
+        exp[out["idx"][m]] = out["val"][m]
+        assert_same("phat row %d" % m, got[m], exp)
+
+
+def test_topk_repeated_steps_stay_exact():
+    """Three iterations on each side's own state: the selection feeds the
+    residual, which feeds the next selection."""
+    from oracle import oracle as orc
+    import synth
+    w = custom(d=120000, M=8, kind="topk", k=1200, eta=1e-2, seed=30)
+    G, E, W = inputs(w)
+    s = GpuState(w, G, E, W)
+    E_r, W_r = E.copy(), W.copy()
+    for t in range(1, 4):
+        Gt = synth.gradients_np(w, t)
+        s.G.copy_(torch_from(Gt))
+        s.fused(t)
+        ref = orc.step(w.as_dict(), np.float32(w.eta), t, Gt, E_r, W_r)
+        compare_step(w, s.host(), ref)
+    s.close()
+
+
+def torch_from(a):
+    from gpu_common import to_dev
+    return to_dev(a)
