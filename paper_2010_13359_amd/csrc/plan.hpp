@@ -32,7 +32,8 @@ struct TopkRow {
     uint32_t iprefix;    // full-row search: ~index bits decided so far
     uint32_t done;       // full-row search finished early (all ties taken)
     uint32_t total;      // selected count found by the tile scan (equals k)
-    uint32_t pad[5];
+    uint32_t n_above;    // keys above the band, counted by the full pass
+    uint32_t pad[4];
 };
 
 constexpr int kTopkTile = 256;            // elements per counting tile (one wave of quads)
@@ -47,6 +48,7 @@ struct TopkScratch {
     int64_t cap = 0;
     uint32_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per 256-element tile
     uint32_t *tile_off = nullptr;   // [M][n_tiles] exclusive prefix of tile_cnt
+    uint32_t *chunk_sum = nullptr;  // [M][n_scan_chunks] tile counts per scan chunk
     int64_t n_tiles = 0;
     int64_t n_chunks = 0;           // sampled chunks per row
     uint32_t n_samples = 0;         // sampled elements per row

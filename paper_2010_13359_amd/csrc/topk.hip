@@ -181,13 +181,16 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                                                       TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
                                                       uint2 *__restrict__ cand, int64_t cap) {
     __shared__ uint2 buf[16 * kTopkTile];
-    __shared__ uint32_t nbuf, base;
+    __shared__ uint32_t nbuf, base, nab;
     const int m = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint32_t lo = rows[m].lo, hi = rows[m].hi;
     const float *g = G + static_cast<int64_t>(m) * ld;
     const float *e = E + static_cast<int64_t>(m) * ld;
-    if (threadIdx.x == 0) nbuf = 0;
+    if (threadIdx.x == 0) {
+        nbuf = 0;
+        nab = 0;
+    }
     __syncthreads();
     const uint64_t below = (uint64_t(1) << lane) - 1;
 #pragma unroll
@@ -205,7 +208,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                 above_n += __popcll(__ballot(valid && keys[k] > hi));
                 cmask |= ((valid && keys[k] >= lo && keys[k] <= hi) ? 1u : 0u) << k;
             }
-            if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
+            if (lane == 0) {
+                tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
+                if (above_n) atomicAdd(&nab, above_n);
+            }
             uint32_t pre = 0, tot = 0;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -228,7 +234,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0) base = nbuf ? atomicAdd(&rows[m].n_cand, nbuf) : 0u;
+    if (threadIdx.x == 0) {
+        base = nbuf ? atomicAdd(&rows[m].n_cand, nbuf) : 0u;
+        if (nab) atomicAdd(&rows[m].n_above, nab);
+    }
     __syncthreads();
     uint2 *crow = cand + static_cast<int64_t>(m) * cap;
     for (uint32_t j = threadIdx.x; j < nbuf; j += kBlock) {
@@ -238,26 +247,20 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
 }
 
 // 4. Exact selection among the candidates (one workgroup per row).  Rows
-// whose band missed are handed to the full-row search.
-__global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows, const uint32_t *__restrict__ tile_cnt,
-                                                      int64_t n_tiles, const uint2 *__restrict__ cand, int64_t cap,
-                                                      int64_t k, uint32_t *__restrict__ hist) {
+// whose band missed are handed to the full-row search.  The candidates' keys
+// lie in [lo, hi]: the digits are taken over key - lo, 11 bits at a time from
+// the top of its width, then (only if the k-th key is shared and not every
+// tie is taken) over ~index.
+__global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows, const uint2 *__restrict__ cand,
+                                                      int64_t cap, int64_t k, uint32_t *__restrict__ hist) {
     __shared__ uint32_t h[kDigitBins];
-    __shared__ unsigned long long red[16];
     __shared__ uint32_t res[3];
     const int m = blockIdx.x;
     const int tid = threadIdx.x;
-    unsigned long long s = 0;
-    for (int64_t t = tid; t < n_tiles; t += 1024) s += tile_cnt[static_cast<int64_t>(m) * n_tiles + t];
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-    if ((tid & 63) == 0) red[tid >> 6] = s;
-    __syncthreads();
-    unsigned long long n_above = 0;
-    for (int w = 0; w < 16; ++w) n_above += red[w];
     const uint32_t n_cand = rows[m].n_cand;
-    const bool ok = n_cand <= cap && n_above < static_cast<unsigned long long>(k) &&
-                    static_cast<unsigned long long>(k) - n_above <= n_cand;
+    const uint64_t n_above = rows[m].n_above;
+    const bool ok = n_cand <= cap && n_above < static_cast<uint64_t>(k) &&
+                    static_cast<uint64_t>(k) - n_above <= n_cand;
     if (!ok) {
         if (tid == 0) {
             rows[m].fallback = 1u;
@@ -270,17 +273,26 @@ __global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows
         for (int b = tid; b < kDigitBins; b += 1024) hm[b] = 0u;
         return;
     }
-    uint32_t rank = static_cast<uint32_t>(static_cast<unsigned long long>(k) - n_above);
-    uint32_t kp = 0, ip = 0, I = 0xFFFFFFFFu;
+    uint32_t rank = static_cast<uint32_t>(static_cast<uint64_t>(k) - n_above);
+    const uint32_t lo = rows[m].lo, span = rows[m].hi - lo;
+    int width = 0;
+    while (width < 32 && (span >> width) != 0u) ++width;  // bits of key - lo
     const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-    for (int pass = 0; pass < 6; ++pass) {
-        const int nb = bins_of(pass);
+    // key digits
+    uint32_t kp = 0;  // decided high bits of key - lo
+    int top = width;
+    uint32_t n_bin = n_cand;
+    while (top > 0) {
+        const int wbits = top < 11 ? top : 11;
+        const int shift = top - wbits;
+        const uint32_t dmask = (1u << wbits) - 1u;
+        const int nb = 1 << wbits;
         for (int b = tid; b < nb; b += 1024) h[b] = 0u;
         __syncthreads();
         for (uint32_t j = tid; j < n_cand; j += 1024) {
-            const uint2 c = crow[j];
-            const uint32_t ni = ~c.y;
-            if (in_play(pass, c.x, ni, kp, ip)) atomicAdd(&h[digit_of(pass, c.x, ni)], 1u);
+            const uint32_t rel = crow[j].x - lo;
+            const bool play = top >= 32 || (rel >> top) == (kp >> top);
+            if (play) atomicAdd(&h[(rel >> shift) & dmask], 1u);
         }
         __syncthreads();
         if (tid < 64) {
@@ -293,16 +305,44 @@ __global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows
             }
         }
         __syncthreads();
-        const uint32_t bin = res[0];
         rank -= res[1];
-        add_prefix(pass, bin, kp, ip);
-        const uint32_t n_bin = res[2];
+        kp |= res[0] << shift;
+        n_bin = res[2];
+        top = shift;
         __syncthreads();
-        if (pass == 2 && rank == n_bin) break;  // every tie at T is taken
-        if (pass == 5) I = ~ip;
+    }
+    const uint32_t T = lo + kp;
+    uint32_t ip = 0, I = 0xFFFFFFFFu;
+    if (rank != n_bin) {
+        // index digits among the ties at T (composite order: smaller index first)
+        for (int pass = 3; pass < 6; ++pass) {
+            const int nb = bins_of(pass);
+            for (int b = tid; b < nb; b += 1024) h[b] = 0u;
+            __syncthreads();
+            for (uint32_t j = tid; j < n_cand; j += 1024) {
+                const uint2 c = crow[j];
+                const uint32_t ni = ~c.y;
+                if (in_play(pass, c.x, ni, T, ip)) atomicAdd(&h[digit_of(pass, c.x, ni)], 1u);
+            }
+            __syncthreads();
+            if (tid < 64) {
+                uint32_t bin = 0, above = 0;
+                wave_find_desc(h, nb, rank, bin, above);
+                if (tid == 0) {
+                    res[0] = bin;
+                    res[1] = above;
+                }
+            }
+            __syncthreads();
+            rank -= res[1];
+            uint32_t kdummy = 0;
+            add_prefix(pass, res[0], kdummy, ip);
+            __syncthreads();
+        }
+        I = ~ip;
     }
     if (tid == 0) {
-        rows[m].T = kp;
+        rows[m].T = T;
         rows[m].I = I;
     }
 }
@@ -414,36 +454,77 @@ __global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restr
     }
 }
 
-// 7. Exclusive scan of the tile counts of each row (one workgroup per row).
-__global__ __launch_bounds__(1024) void k_topk_tile_scan(TopkRow *__restrict__ rows,
-                                                         const uint32_t *__restrict__ tile_cnt,
-                                                         uint32_t *__restrict__ tile_off, int64_t n_tiles) {
-    __shared__ uint32_t wsum[16];
-    const int m = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int64_t per = (n_tiles + 1023) / 1024;
-    const int64_t a = static_cast<int64_t>(tid) * per;
-    const int64_t b = a + per < n_tiles ? a + per : n_tiles;
-    const uint32_t *cr = tile_cnt + static_cast<int64_t>(m) * n_tiles;
-    uint32_t *orow = tile_off + static_cast<int64_t>(m) * n_tiles;
-    uint32_t s = 0;
-    for (int64_t t = a; t < b; ++t) s += cr[t];
-    uint32_t incl = s;
+// 7. Exclusive scan of the tile counts of each row, in chunks of 4096 tiles:
+// each workgroup scans its chunk (4 consecutive counts per thread) and
+// records the chunk's total; a second kernel adds the totals of the earlier
+// chunks of the row.
+constexpr int kScanChunk = 4096;
+
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *wsum, uint32_t &total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t incl = v;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t v = __shfl_up(incl, o);
-        if (lane >= o) incl += v;
+        const uint32_t x = __shfl_up(incl, o);
+        if (lane >= o) incl += x;
     }
     if (lane == 63) wsum[wave] = incl;
     __syncthreads();
-    uint32_t wbase = 0;
-    for (int w = 0; w < wave; ++w) wbase += wsum[w];
-    uint32_t run = wbase + incl - s;
-    for (int64_t t = a; t < b; ++t) {
-        orow[t] = run;
-        run += cr[t];
+    uint32_t wbase = 0, tot = 0;
+    for (int w = 0; w < 16; ++w) {
+        if (w < wave) wbase += wsum[w];
+        tot += wsum[w];
     }
-    if (tid == 1023) rows[m].total = run;
+    total = tot;
+    return wbase + incl - v;
+}
+
+__global__ __launch_bounds__(1024) void k_topk_scan_local(const uint32_t *__restrict__ tile_cnt,
+                                                          uint32_t *__restrict__ tile_off,
+                                                          uint32_t *__restrict__ chunk_sum, int64_t n_tiles,
+                                                          int64_t n_chunks) {
+    __shared__ uint32_t wsum[16];
+    const int m = blockIdx.y;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kScanChunk + 4 * threadIdx.x;
+    const uint32_t *cr = tile_cnt + static_cast<int64_t>(m) * n_tiles;
+    uint32_t *orow = tile_off + static_cast<int64_t>(m) * n_tiles;
+    uint32_t c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = (t0 + j < n_tiles) ? cr[t0 + j] : 0u;
+    uint32_t total;
+    uint32_t run = block_exclusive_scan(c[0] + c[1] + c[2] + c[3], wsum, total);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        if (t0 + j < n_tiles) orow[t0 + j] = run;
+        run += c[j];
+    }
+    if (threadIdx.x == 0) chunk_sum[static_cast<int64_t>(m) * n_chunks + blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(1024) void k_topk_scan_add(TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_off,
+                                                        const uint32_t *__restrict__ chunk_sum, int64_t n_tiles,
+                                                        int64_t n_chunks) {
+    __shared__ uint32_t base;
+    const int m = blockIdx.y;
+    const int64_t c = blockIdx.x;
+    if (threadIdx.x < 64) {
+        uint32_t s = 0;
+        for (int64_t j = threadIdx.x; j < c; j += 64) s += chunk_sum[static_cast<int64_t>(m) * n_chunks + j];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+        if (threadIdx.x == 0) {
+            base = s;
+            if (c == n_chunks - 1) rows[m].total = s + chunk_sum[static_cast<int64_t>(m) * n_chunks + c];
+        }
+    }
+    __syncthreads();
+    const uint32_t b = base;
+    if (b == 0) return;
+    uint32_t *orow = tile_off + static_cast<int64_t>(m) * n_tiles;
+    const int64_t t0 = c * kScanChunk + 4 * threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (t0 + j < n_tiles) orow[t0 + j] += b;
 }
 
 // Server side: scatter the messages (unpack), or add them in worker order.
@@ -500,6 +581,9 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
         e = hipMalloc(reinterpret_cast<void **>(&S.tile_cnt), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.tile_off), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
+    const int64_t nsc = (S.n_tiles + kScanChunk - 1) / kScanChunk;
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.chunk_sum), M * static_cast<size_t>(nsc) * sizeof(uint32_t));
     return e;
 }
 
@@ -510,6 +594,7 @@ void topk_free(dqgan_plan_s &P) {
     (void)hipFree(S.cand);
     (void)hipFree(S.tile_cnt);
     (void)hipFree(S.tile_off);
+    (void)hipFree(S.chunk_sum);
     S = TopkScratch{};
 }
 
@@ -525,8 +610,7 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(64), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
     hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + 15) / 16), M), dim3(kBlock), 0, st, G, E,
                        eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
-    hipLaunchKernelGGL(k_topk_select, dim3(M), dim3(1024), 0, st, S.rows, S.tile_cnt, S.n_tiles, S.cand, S.cap, D.k,
-                       S.hist);
+    hipLaunchKernelGGL(k_topk_select, dim3(M), dim3(1024), 0, st, S.rows, S.cand, S.cap, D.k, S.hist);
     hipLaunchKernelGGL(k_topk_count, dim3(64, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, S.tile_cnt, S.n_tiles);
     for (int pass = 0; pass < 6; ++pass) {
         hipLaunchKernelGGL(k_topk_fb_hist, dim3(kFbBlocks, M), dim3(kBlock), 0, st, pass, G, E, eta, D.d, D.ld, S.rows,
@@ -535,7 +619,11 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     }
     hipLaunchKernelGGL(k_topk_fb_recount, dim3(256, M), dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows,
                        S.tile_cnt);
-    hipLaunchKernelGGL(k_topk_tile_scan, dim3(M), dim3(1024), 0, st, S.rows, S.tile_cnt, S.tile_off, S.n_tiles);
+    const int64_t nsc = (S.n_tiles + kScanChunk - 1) / kScanChunk;
+    hipLaunchKernelGGL(k_topk_scan_local, dim3(static_cast<unsigned>(nsc), M), dim3(1024), 0, st, S.tile_cnt,
+                       S.tile_off, S.chunk_sum, S.n_tiles, nsc);
+    hipLaunchKernelGGL(k_topk_scan_add, dim3(static_cast<unsigned>(nsc), M), dim3(1024), 0, st, S.rows, S.tile_off,
+                       S.chunk_sum, S.n_tiles, nsc);
     return hipGetLastError();
 }
 
