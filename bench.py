@@ -191,7 +191,7 @@ def main():
     achieved = b_alg / (t_apply * 1e-3) / 1e9
     step_ach = b_alg / (ms_step * 1e-3) / 1e9
     kernel_key = "apply_C%d" % w.index
-    traffic = traffic_record(kernel_key, "topk" if w.kind == "topk" else "dense")
+    traffic = traffic_record(kernel_key, "dense")  # the apply pass of every compressor is in dense.hip
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
