@@ -38,21 +38,35 @@ __global__ __launch_bounds__(kBlock) void k_segment_partials(const float *__rest
     const int64_t q0 = lo >> 2, q1 = (hi + 3) >> 2;
     double acc[4] = {0.0, 0.0, 0.0, 0.0};
     float mx = 0.0f;
-    for (int64_t q = q0 + threadIdx.x; q < q1; q += kBlock) {
-        const f32x4 gv = ld4(g + 4 * q);
-        const f32x4 ev = ld4(e + 4 * q);
+    // Four quads per thread per trip, all eight loads issued before use.
+    constexpr int U = 4;
+    for (int64_t qb = q0 + threadIdx.x; qb < q1; qb += U * kBlock) {
+        f32x4 gv[U], ev[U];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const int64_t i = 4 * q + c;
-            const float p = add_rn(mul_rn(eta, elem(gv, c)), elem(ev, c));
-            const bool in = (i >= lo) && (i < hi);
-            if (NORM == DQGAN_L1) {
-                acc[c] += in ? static_cast<double>(fabsf(p)) : 0.0;
-            } else if (NORM == DQGAN_L2) {
-                const double pd = static_cast<double>(p);
-                acc[c] += in ? pd * pd : 0.0;  // the product is exact in binary64
-            } else {
-                mx = in ? fmaxf(mx, fabsf(p)) : mx;
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = qb + u * kBlock;
+            if (q < q1) {
+                gv[u] = ld_stream(g + 4 * q);
+                ev[u] = ld_stream(e + 4 * q);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int64_t q = qb + u * kBlock;
+            if (q >= q1) break;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int64_t i = 4 * q + c;
+                const float p = add_rn(mul_rn(eta, elem(gv[u], c)), elem(ev[u], c));
+                const bool in = (i >= lo) && (i < hi);
+                if (NORM == DQGAN_L1) {
+                    acc[c] += in ? static_cast<double>(fabsf(p)) : 0.0;
+                } else if (NORM == DQGAN_L2) {
+                    const double pd = static_cast<double>(p);
+                    acc[c] += in ? pd * pd : 0.0;  // the product is exact in binary64
+                } else {
+                    mx = in ? fmaxf(mx, fabsf(p)) : mx;
+                }
             }
         }
     }

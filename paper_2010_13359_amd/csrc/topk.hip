@@ -193,12 +193,23 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     }
     __syncthreads();
     const uint64_t below = (uint64_t(1) << lane) - 1;
+    // The wave's four tiles are loaded before any of them is examined.
+    f32x4 gvs[4], evs[4];
 #pragma unroll
     for (int it = 0; it < 4; ++it) {
         const int64_t tile = static_cast<int64_t>(blockIdx.x) * 16 + it * 4 + wave;
         if (tile < n_tiles) {
             const int64_t i0 = tile * kTopkTile + 4 * lane;
-            const f32x4 gv = ld_stream(g + i0), ev = ld_stream(e + i0);
+            gvs[it] = ld_stream(g + i0);
+            evs[it] = ld_stream(e + i0);
+        }
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+        const int64_t tile = static_cast<int64_t>(blockIdx.x) * 16 + it * 4 + wave;
+        if (tile < n_tiles) {
+            const int64_t i0 = tile * kTopkTile + 4 * lane;
+            const f32x4 gv = gvs[it], ev = evs[it];
             uint32_t keys[4];
             uint32_t above_n = 0, cmask = 0;
 #pragma unroll
