@@ -249,6 +249,23 @@ void oracle_decode_segment(int32_t kind, int64_t n, const uint16_t *signs, const
     }
 }
 
+/* The m-bit code of Appendix A: q(v_i, s) takes one of the 2k+1 values
+ * -B_k .. B_k with k = 2^(m-1) - 1, which m bits hold as sign and magnitude:
+ * bit m-1 is the sign, bits 0..m-2 the level r (reading: B_r = r / k, so that
+ * the rounding rule is the one of equation (qsgd) with k levels). */
+void oracle_mbit_fields(int64_t n, int32_t mbits, const uint8_t *bits, const uint16_t *levels, uint16_t *fields) {
+    for (int64_t i = 0; i < n; ++i)
+        fields[i] = (uint16_t)(((uint32_t)bits[i] << (mbits - 1)) | levels[i]);
+}
+
+void oracle_mbit_split(int64_t n, int32_t mbits, const uint16_t *fields, uint16_t *signs, uint16_t *levels) {
+    uint16_t mask = (uint16_t)((1u << (mbits - 1)) - 1u);
+    for (int64_t i = 0; i < n; ++i) {
+        signs[i] = (uint16_t)(fields[i] >> (mbits - 1));
+        levels[i] = (uint16_t)(fields[i] & mask);
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Server: qhat = (1/M) sum_m phat^(m) (Algorithm 2).  The running sum S
  * starts at phat^(0) and adds phat^(1), ..., phat^(M-1) in that order. */
@@ -278,7 +295,8 @@ void oracle_extrapolate(int64_t d, float eta, const float *w, const float *g, co
 
 /* ------------------------------------------------------------------------ */
 /* One full iteration over M workers (rows of stride ld) for the compressor
- * `kind` (0 sign, 1 s-level quantizer, 2 top-k, 3 identity).
+ * `kind` (0 sign, 1 s-level quantizer, 2 top-k, 3 identity, 4 the m-bit
+ * sign-magnitude quantizer of Appendix A with `levels` = m bits).
  *
  * In: G (the fresh gradients), E (e_{t-1}), W (w_{t-1}).
  * Out: E (e_t), W (w_t), WX (next evaluation points), the message planes and
@@ -303,6 +321,8 @@ int oracle_step(const oracle_desc *D, float eta, uint32_t t, const float *G, flo
     int32_t M = D->M;
     if (d < 1 || ld < d || M < 1) return -1;
     int32_t bits_per_level = (D->levels == 255) ? 8 : (D->levels == 15) ? 4 : 0;
+    int32_t mbits = (D->kind == 4) ? D->levels : 0;           /* Appendix A: m bits per code */
+    int32_t mlevels = mbits ? (1 << (mbits - 1)) - 1 : 0;     /* k = 2^(m-1) - 1 */
     float *p = (float *)malloc((size_t)d * sizeof(float));
     float *phat = (float *)malloc((size_t)d * sizeof(float));
     float *dec = (float *)malloc((size_t)d * sizeof(float));
@@ -349,6 +369,28 @@ int oracle_step(const oracle_desc *D, float eta, uint32_t t, const float *G, flo
                 int64_t a = D->seg_offsets[j], b = D->seg_offsets[j + 1];
                 oracle_decode_segment(D->kind, b - a, fs + a, fl + a, scales[(int64_t)m * D->n_seg + j],
                                       D->levels, dec + a);
+            }
+        } else if (D->kind == 4) {
+            int64_t rw = ld * mbits / 32;  /* code words per row */
+            for (int32_t j = 0; j < D->n_seg; ++j) {
+                int64_t a = D->seg_offsets[j], b = D->seg_offsets[j + 1];
+                int64_t n = b - a;
+                float sc;
+                if (scales_in) sc = scales_in[(int64_t)m * D->n_seg + j];
+                else if (D->norm == 3) sc = oracle_scale_linf(n, p + a);
+                else sc = oracle_scale_l2(n, p + a);
+                scales[(int64_t)m * D->n_seg + j] = sc;
+                oracle_qsgd_encode(n, a, p + a, sc, mlevels, D->seed, m, t, bits + a, lv + a, phat + a, e + a);
+            }
+            /* push: one m-bit sign-magnitude code per element */
+            oracle_mbit_fields(d, mbits, bits, lv, fs);
+            oracle_pack_bits(d, mbits, fs, level_words + (int64_t)m * rw, rw);
+            /* pull: the server splits and decodes the codes */
+            oracle_unpack_bits(d, mbits, level_words + (int64_t)m * rw, fl);
+            oracle_mbit_split(d, mbits, fl, fs, lv);
+            for (int32_t j = 0; j < D->n_seg; ++j) {
+                int64_t a = D->seg_offsets[j], b = D->seg_offsets[j + 1];
+                oracle_decode_segment(1, b - a, fs + a, lv + a, scales[(int64_t)m * D->n_seg + j], mlevels, dec + a);
             }
         } else if (D->kind == 2) {
             if (oracle_topk(d, D->k, p, idx + (int64_t)m * D->k, val + (int64_t)m * D->k, phat, e) != 0) {

@@ -17,7 +17,7 @@ SRC = os.path.join(_HERE, "dqgan_oracle.c")
 LIB = os.path.join(_HERE, "libdqgan_oracle.so")
 CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
 
-KIND = {"sign": 0, "qsgd": 1, "topk": 2, "identity": 3}
+KIND = {"sign": 0, "qsgd": 1, "topk": 2, "identity": 3, "mbit": 4}
 NORM = {"l1": 1, "l2": 2, "linf": 3}
 
 
@@ -65,6 +65,8 @@ def lib():
         L.oracle_pack_bits.argtypes = [i64, i32, P, P, i64]
         L.oracle_unpack_bits.argtypes = [i64, i32, P, P]
         L.oracle_decode_segment.argtypes = [i32, i64, P, P, f32, i32, P]
+        L.oracle_mbit_fields.argtypes = [i64, i32, P, P, P]
+        L.oracle_mbit_split.argtypes = [i64, i32, P, P, P]
         L.oracle_aggregate.argtypes = [i32, i64, i64, P, P]
         L.oracle_omd_update.argtypes = [i64, P, P]
         L.oracle_extrapolate.argtypes = [i64, f32, P, P, P, P]
@@ -161,6 +163,23 @@ def decode_segment(kind, signs, levels, s, nlevels=0):
     return out
 
 
+def mbit_fields(bits, levels, mbits):
+    """Appendix A's m-bit sign-magnitude codes of (sign bit, level)."""
+    b = np.ascontiguousarray(bits, dtype=np.uint8)
+    lv = np.ascontiguousarray(levels, dtype=np.uint16)
+    f = np.empty(b.size, np.uint16)
+    lib().oracle_mbit_fields(b.size, mbits, _ptr(b), _ptr(lv), _ptr(f))
+    return f
+
+
+def mbit_split(fields, mbits):
+    f = np.ascontiguousarray(fields, dtype=np.uint16)
+    sg = np.empty(f.size, np.uint16)
+    lv = np.empty(f.size, np.uint16)
+    lib().oracle_mbit_split(f.size, mbits, _ptr(f), _ptr(sg), _ptr(lv))
+    return sg, lv
+
+
 def aggregate(phat, d):
     phat = _f32(phat)
     M, ld = phat.shape
@@ -183,7 +202,9 @@ def extrapolate(eta, w, g, e):
 
 
 def wire_words(kind, ld, levels=0):
-    """Words per row of the sign plane and of the level plane."""
+    """Words per row of the sign plane and of the level (code) plane."""
+    if kind == "mbit":
+        return 0, ld * levels // 32
     b = {255: 8, 15: 4}.get(levels, 0)
     sign = ld // 32 if kind in ("sign", "qsgd") else 0
     lev = ld * b // 32 if kind == "qsgd" else 0

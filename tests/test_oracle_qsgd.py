@@ -32,7 +32,7 @@ def _bin_variance(v, sigma, s):
     return (a - lo) * (hi - a)
 
 
-@pytest.mark.parametrize("s,norm", [(15, "l2"), (255, "l2"), (15, "linf")])
+@pytest.mark.parametrize("s,norm", [(15, "l2"), (255, "l2"), (15, "linf"), (7, "linf"), (127, "linf")])
 def test_unbiased_and_exact_variance(oracle_mod, s, norm):
     rng = np.random.default_rng(s)
     d = 600

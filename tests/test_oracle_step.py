@@ -80,7 +80,8 @@ def test_identity_single_worker_is_omd(oracle_mod):
 
 
 @pytest.mark.parametrize("kind,extra", [("sign", {}), ("qsgd", {"levels": 15}), ("qsgd", {"levels": 255}),
-                                        ("qsgd", {"levels": 15, "norm": "linf"}), ("topk", {"k": 97})])
+                                        ("qsgd", {"levels": 15, "norm": "linf"}), ("topk", {"k": 97}),
+                                        ("mbit", {"levels": 8, "norm": "linf"}), ("mbit", {"levels": 4, "norm": "l2"})])
 def test_error_corrected_sequence(oracle_mod, kind, extra):
     """Appendix B, equation tilde: w~_t = w_t - (1/M) sum_m e_t^(m) obeys
     w~_t = w~_{t-1} - (eta/M) sum_m g_t^(m) for any compressor.  Checked in
