@@ -53,6 +53,8 @@ def wire_bits(w):
         return 1.0
     if w.kind == "qsgd":
         return 1.0 + (8 if w.levels == 255 else 4)
+    if w.kind == "mbit":
+        return float(w.levels)
     if w.kind == "topk":
         return 64.0 * w.k / w.d
     return 32.0
@@ -68,7 +70,9 @@ def algorithmic_bytes(w):
 
 def workload_label(w):
     comp = {"sign": "scaled sign (L1 mean)", "qsgd": "s-level quantizer s=%d %s" % (w.levels, w.norm.upper()),
-            "topk": "top-k k=%d" % w.k, "identity": "identity"}[w.kind]
+            "topk": "top-k k=%d" % w.k, "identity": "identity",
+            "mbit": "%d-bit sign-magnitude quantizer (k=%d) %s" % (w.levels, (1 << (w.levels - 1)) - 1,
+                                                                  w.norm.upper())}[w.kind]
     return "C%d %s: d=%d, M=%d workers, %s, %d segments, eta=%g" % (w.index, w.name, w.d, w.M, comp, w.n_seg, w.eta)
 
 
@@ -101,7 +105,7 @@ def cpu_baseline(w, target_elems=4_000_000):
     n = offs[-1]
     nseg = len(offs) - 1
     sub = custom(d=n, M=w.M, kind=w.kind, levels=w.levels, k=max(1, w.k * n // w.d) if w.k else 0,
-                 seg_offsets=offs if w.kind != "topk" else None, norm=w.norm if w.kind in ("sign", "qsgd") else None,
+                 seg_offsets=offs if w.kind != "topk" else None, norm=w.norm if w.kind in ("sign", "qsgd", "mbit") else None,
                  eta=w.eta, seed=w.seed, law=w.law, group_scale=w.group_scale[:nseg])
     G = synth.gradients_np(sub, 1)
     E = np.zeros((sub.M, sub.ld), np.float32)
@@ -122,7 +126,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, help="workload index C0..C4 (default C3)")
+    ap.add_argument("--config", type=int, default=3, help="workload index C0..C6 (default C3)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of 1 GiB (counter calibration)")

@@ -65,7 +65,10 @@ typedef enum {
                            (Section 2.4, sign with a scaling factor)         */
     DQGAN_QSGD = 1,     /* s-level stochastic quantizer, equation (qsgd)    */
     DQGAN_TOPK = 2,     /* k largest magnitudes (Theorem 1)                 */
-    DQGAN_IDENTITY = 3  /* Q = id (delta = 1): the uncompressed special case */
+    DQGAN_IDENTITY = 3, /* Q = id (delta = 1): the uncompressed special case */
+    DQGAN_MBIT = 4      /* m-bit sign-magnitude stochastic quantizer with
+                           k = 2^(m-1) - 1 uniform levels (Appendix A); with
+                           DQGAN_LINF the compressor of the experiments     */
 } dqgan_kind;
 
 typedef enum {
@@ -84,9 +87,10 @@ typedef struct {
                                      seg_offsets[0] = 0, seg_offsets[n_seg] = d;
                                      copied by dqgan_plan_create                   */
     int32_t kind;                 /* dqgan_kind                                     */
-    int32_t norm;                 /* SIGN: DQGAN_L1; QSGD: DQGAN_L2 or DQGAN_LINF;
-                                     TOPK, IDENTITY: DQGAN_NORM_NONE               */
-    int32_t levels;               /* QSGD s: 255 (8-bit level field) or 15 (4-bit) */
+    int32_t norm;                 /* SIGN: DQGAN_L1; QSGD, MBIT: DQGAN_L2 or
+                                     DQGAN_LINF; TOPK, IDENTITY: DQGAN_NORM_NONE   */
+    int32_t levels;               /* QSGD s: 255 (8-bit level field) or 15 (4-bit);
+                                     MBIT: code bits m, 8 or 4 (k = 127 or 7)      */
     int32_t reserved;             /* must be 0                                      */
     int64_t k;                    /* TOPK: 1 <= k <= d, d < 2^32, M <= 64
                                      (larger M: DQGAN_EUNSUPPORTED)                 */
@@ -100,8 +104,12 @@ typedef struct dqgan_plan_s *dqgan_plan;
  *   (i & 31) of word i >> 5; 1 means the sign bit of p_i is set.
  * Level plane (QSGD): uint32 [M][ld*b/32] with b = 8 (s = 255) or 4 (s = 15);
  *   element i is the b-bit field at bit b*(i mod (32/b)) of word i/(32/b).
- * Scales (SIGN, QSGD): fp32 [M][n_seg], the scale (SIGN) or sigma (QSGD) of
- *   segment j of worker m.
+ * Code plane (MBIT): the level plane holds one m-bit code per element,
+ *   uint32 [M][ld*m/32], element i in the m-bit field at bit m*(i mod (32/m))
+ *   of word i/(32/m); bit m-1 of a code is the sign bit, bits 0..m-2 the
+ *   level.  The sign plane is not used.
+ * Scales (SIGN, QSGD, MBIT): fp32 [M][n_seg], the scale (SIGN) or sigma
+ *   (QSGD, MBIT) of segment j of worker m.
  * val/idx (TOPK): fp32 and uint32 [M][k]; the selected p_i and their indices
  *   i, in ascending i.  (IDENTITY: val is the dense fp32 [M][ld] p-hat = p.)
  * Unused planes may be NULL. */
@@ -141,22 +149,24 @@ dqgan_status dqgan_wire_bytes(dqgan_plan plan, size_t *sign, size_t *level, size
  * word i & 3; r = fl(|p| * fl(s/sigma)), l = min(floor(r), s), level =
  * min(l + [u < r - l], s) (l = s rounds no further); p-hat =
  * copysign(fl(level * fl(sigma/s)), p); sigma = 0 gives level 0.
+ * MBIT: the QSGD rule with s = k = 2^(m-1) - 1 levels.
  * SIGN: p-hat = -scale if the sign bit of p is set, else +scale.
  * TOPK: the k largest |p| (ties to the lower index); p-hat = p there, 0
  * elsewhere. */
 dqgan_status dqgan_compress_ef(dqgan_plan plan, float eta, uint32_t t, const float *G, float *E,
                                const float *scales_in, const dqgan_wire *out, void *stream);
 
-/* Pack per-element codes into the message planes (SIGN, QSGD).
- *   codes: [M][ld] uint16; bit 15 = sign bit, bits 0..14 = level (QSGD;
- *   must be <= s).  scales: [M][n_seg], copied to out->scale.
+/* Pack per-element codes into the message planes (SIGN, QSGD, MBIT).
+ *   codes: [M][ld] uint16; bit 15 = sign bit, bits 0..14 = level (QSGD, MBIT;
+ *   must be <= s, resp. k).  scales: [M][n_seg], copied to out->scale.
  * TOPK and IDENTITY return DQGAN_EUNSUPPORTED. */
 dqgan_status dqgan_pack(dqgan_plan plan, const uint16_t *codes, const float *scales, const dqgan_wire *out,
                         void *stream);
 
 /* Decode the M messages to the dense p-hat [M][ld] (what the server sees
  * after pulling them).  SIGN: +-scale; QSGD: copysign(fl(level * fl(sigma/s)),
- * sign); TOPK: val at idx, 0 elsewhere; IDENTITY: val. */
+ * sign); MBIT: the same with s = k; TOPK: val at idx, 0 elsewhere; IDENTITY:
+ * val. */
 dqgan_status dqgan_unpack(dqgan_plan plan, const dqgan_wire *in, float *Phat, void *stream);
 
 /* Server average (Algorithm 2): Qhat_i = fl(S_i / M) with

@@ -64,6 +64,10 @@ dqgan_status validate_desc(const dqgan_desc *D) {
         case DQGAN_IDENTITY:
             if (D->norm != DQGAN_NORM_NONE) return DQGAN_EINVAL;
             break;
+        case DQGAN_MBIT:
+            if (D->norm != DQGAN_L2 && D->norm != DQGAN_LINF) return DQGAN_EINVAL;
+            if (D->levels != 8 && D->levels != 4) return DQGAN_EINVAL;
+            break;
         default:
             return DQGAN_EINVAL;
     }
@@ -88,7 +92,7 @@ void free_plan_memory(dqgan_plan_s *P) {
     dq::topk_free(*P);
 }
 
-bool dense_kind(int k) { return k == DQGAN_SIGN || k == DQGAN_QSGD || k == DQGAN_IDENTITY; }
+bool dense_kind(int k) { return k == DQGAN_SIGN || k == DQGAN_QSGD || k == DQGAN_IDENTITY || k == DQGAN_MBIT; }
 
 dqgan_status check_wire(const dqgan_plan_s *P, const dqgan_wire *w, bool need_scale) {
     if (!w) return DQGAN_EINVAL;
@@ -99,6 +103,10 @@ dqgan_status check_wire(const dqgan_plan_s *P, const dqgan_wire *w, bool need_sc
             break;
         case DQGAN_QSGD:
             DQ_TRY(need(w->sign));
+            DQ_TRY(need(w->level));
+            if (need_scale) DQ_TRY(need(w->scale));
+            break;
+        case DQGAN_MBIT:
             DQ_TRY(need(w->level));
             if (need_scale) DQ_TRY(need(w->scale));
             break;
@@ -142,7 +150,8 @@ dqgan_status dqgan_plan_create(const dqgan_desc *desc, dqgan_plan *out) {
     else
         P->offsets = {0, d};
     P->desc.seg_offsets = nullptr;  // the host copy lives in P->offsets
-    P->level_bits = desc->kind == DQGAN_QSGD ? (desc->levels == 255 ? 8 : 4) : 0;
+    P->level_bits = desc->kind == DQGAN_QSGD ? (desc->levels == 255 ? 8 : 4) : desc->kind == DQGAN_MBIT ? desc->levels : 0;
+    P->level_count = desc->kind == DQGAN_QSGD ? desc->levels : desc->kind == DQGAN_MBIT ? (1 << (desc->levels - 1)) - 1 : 0;
     P->n_tiles = desc->ld / 1024;
     if (hipGetDevice(&P->device) != hipSuccess) {
         delete P;
@@ -214,9 +223,9 @@ dqgan_status dqgan_wire_bytes(dqgan_plan P, size_t *sign, size_t *level, size_t 
     if (!P) return DQGAN_EINVAL;
     const dqgan_desc &D = P->desc;
     const size_t M = static_cast<size_t>(D.M), ld = static_cast<size_t>(D.ld);
-    const bool coded = D.kind == DQGAN_SIGN || D.kind == DQGAN_QSGD;
-    if (sign) *sign = coded ? M * (ld / 32) * 4 : 0;
-    if (level) *level = D.kind == DQGAN_QSGD ? M * (ld * P->level_bits / 32) * 4 : 0;
+    const bool coded = D.kind == DQGAN_SIGN || D.kind == DQGAN_QSGD || D.kind == DQGAN_MBIT;
+    if (sign) *sign = (D.kind == DQGAN_SIGN || D.kind == DQGAN_QSGD) ? M * (ld / 32) * 4 : 0;
+    if (level) *level = (D.kind == DQGAN_QSGD || D.kind == DQGAN_MBIT) ? M * (ld * P->level_bits / 32) * 4 : 0;
     if (scale) *scale = coded ? M * static_cast<size_t>(D.n_seg) * 4 : 0;
     if (val) *val = D.kind == DQGAN_TOPK ? M * static_cast<size_t>(D.k) * 4 : D.kind == DQGAN_IDENTITY ? M * ld * 4 : 0;
     if (idx) *idx = D.kind == DQGAN_TOPK ? M * static_cast<size_t>(D.k) * 4 : 0;
@@ -244,7 +253,8 @@ dqgan_status dqgan_compress_ef(dqgan_plan P, float eta, uint32_t t, const float 
 dqgan_status dqgan_pack(dqgan_plan P, const uint16_t *codes, const float *scales, const dqgan_wire *out,
                         void *stream) {
     if (!P) return DQGAN_EINVAL;
-    if (P->desc.kind != DQGAN_SIGN && P->desc.kind != DQGAN_QSGD) return DQGAN_EUNSUPPORTED;
+    if (P->desc.kind != DQGAN_SIGN && P->desc.kind != DQGAN_QSGD && P->desc.kind != DQGAN_MBIT)
+        return DQGAN_EUNSUPPORTED;
     DQ_TRY(need(codes));
     DQ_TRY(need(scales));
     DQ_TRY(check_wire(P, out, true));

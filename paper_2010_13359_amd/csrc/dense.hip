@@ -19,7 +19,7 @@ namespace dq {
 
 namespace {
 
-enum { kSign = DQGAN_SIGN, kQsgd = DQGAN_QSGD, kTopk = DQGAN_TOPK, kIdentity = DQGAN_IDENTITY };
+enum { kSign = DQGAN_SIGN, kQsgd = DQGAN_QSGD, kTopk = DQGAN_TOPK, kIdentity = DQGAN_IDENTITY, kMbit = DQGAN_MBIT };
 
 // ---------------------------------------------------------------------------
 // Pass 1: segment statistics.
@@ -123,7 +123,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int lev
     }
     if (scale_out) scale_out[tid] = sc;
     float2 c;
-    if (kind == kQsgd) {
+    if (kind == kQsgd || kind == kMbit) {
         const double sd = static_cast<double>(sc), ld = static_cast<double>(levels);
         if (sc > 0.0f && sc <= 3.402823466e38f) {
             c.x = static_cast<float>(ld / sd);
@@ -158,7 +158,7 @@ __device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, f
     o.sign_nib = 0u;
     o.levels = 0u;
     u32x4 rnd;
-    if (KIND == kQsgd) {
+    if (KIND == kQsgd || KIND == kMbit) {
         const uint64_t blk = static_cast<uint64_t>(i0) >> 2;
         rnd = philox4x32_10(static_cast<uint32_t>(blk), static_cast<uint32_t>(m), t, static_cast<uint32_t>(blk >> 32),
                             k0, k1);
@@ -177,7 +177,7 @@ __device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, f
             if (KIND == kSign) {
                 const float sc = crow[js[c]].x;
                 q = neg ? -sc : sc;
-            } else if (KIND == kQsgd) {
+            } else if (KIND == kQsgd || KIND == kMbit) {
                 const float2 cs = crow[js[c]];
                 const float a = fabsf(p);
                 if (cs.x > 0.0f && a > 0.0f) {
@@ -287,6 +287,17 @@ __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, u
             const uint16_t h = static_cast<uint16_t>((l & 0xFu) | ((l >> 4) & 0xF0u) | ((l >> 8) & 0xF00u) |
                                                      ((l >> 12) & 0xF000u));
             reinterpret_cast<uint16_t *>(level_row)[q] = h;
+        }
+    }
+    if (KIND == kMbit) {
+        // m-bit sign-magnitude codes: the sign bit on top of each field
+        const uint32_t nib = cq.sign_nib, l = cq.levels;
+        if (LB == 8) {
+            level_row[q] = l | ((nib & 1u) << 7) | ((nib & 2u) << 14) | ((nib & 4u) << 21) | ((nib & 8u) << 28);
+        } else {
+            const uint32_t h = (l & 0x7u) | ((l >> 4) & 0x70u) | ((l >> 8) & 0x700u) | ((l >> 12) & 0x7000u) |
+                               ((nib & 1u) << 3) | ((nib & 2u) << 6) | ((nib & 4u) << 9) | ((nib & 8u) << 12);
+            reinterpret_cast<uint16_t *>(level_row)[q] = static_cast<uint16_t>(h);
         }
     }
     if (KIND == kIdentity) st4(val_row + 4 * q, cq.phat);
@@ -527,8 +538,20 @@ __device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_r
         for (int c = 0; c < 4; ++c) set_elem(out, c, (i0 + c < d) ? elem(v, c) : 0.0f);
         return out;
     }
-    const uint32_t nib = (sign_row[q >> 3] >> (4 * (q & 7))) & 0xFu;
-    uint32_t lev = 0u;
+    uint32_t nib = 0u, lev = 0u;
+    if (KIND == kMbit) {
+        if (LB == 8) {
+            const uint32_t wv = level_row[q];
+            lev = wv & 0x7F7F7F7Fu;
+            nib = ((wv >> 7) & 1u) | ((wv >> 14) & 2u) | ((wv >> 21) & 4u) | ((wv >> 28) & 8u);
+        } else {
+            const uint32_t h = reinterpret_cast<const uint16_t *>(level_row)[q];
+            lev = (h & 0x7u) | ((h & 0x70u) << 4) | ((h & 0x700u) << 8) | ((h & 0x7000u) << 12);
+            nib = ((h >> 3) & 1u) | ((h >> 6) & 2u) | ((h >> 9) & 4u) | ((h >> 12) & 8u);
+        }
+    } else {
+        nib = (sign_row[q >> 3] >> (4 * (q & 7))) & 0xFu;
+    }
     if (KIND == kQsgd) {
         if (LB == 8) {
             lev = level_row[q];
@@ -627,7 +650,7 @@ __global__ __launch_bounds__(kBlock) void k_omd(const float *__restrict__ Qhat, 
     }
 }
 
-template <int LB>
+template <int LB, int KIND>
 __global__ __launch_bounds__(kBlock) void k_pack(const uint16_t *__restrict__ codes, uint32_t *__restrict__ sign_plane,
                                                  uint32_t *__restrict__ level_plane, RowArgs a) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
@@ -638,15 +661,17 @@ __global__ __launch_bounds__(kBlock) void k_pack(const uint16_t *__restrict__ co
     QuadCodes cq;
     cq.sign_nib = 0u;
     cq.levels = 0u;
-    const uint32_t fmask = LB == 8 ? 0xFFu : 0xFu;
+    const uint32_t fmask = KIND == kMbit ? (LB == 8 ? 0x7Fu : 0x7u) : (LB == 8 ? 0xFFu : 0xFu);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         if (i0 + c >= a.d) continue;
         cq.sign_nib |= ((c4[c] >> 15) & 1u) << c;
         cq.levels |= (c4[c] & fmask) << (8 * c);
     }
-    if (LB == 0)
+    if (KIND == kSign)
         store_message<kSign, 0>(sign_plane + m * a.sign_words, nullptr, nullptr, q, cq);
+    else if (KIND == kMbit)
+        store_message<kMbit, LB>(nullptr, level_plane + m * a.level_words, nullptr, q, cq);
     else
         store_message<kQsgd, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, nullptr, q, cq);
 }
@@ -674,7 +699,7 @@ RowArgs row_args(const dqgan_plan_s &P, float eta, uint32_t t) {
     a.ld = P.desc.ld;
     a.M = P.desc.M;
     a.n_seg = P.desc.n_seg;
-    a.s = P.desc.levels;
+    a.s = P.level_count;
     a.k0 = static_cast<uint32_t>(P.desc.seed);
     a.k1 = static_cast<uint32_t>(P.desc.seed >> 32);
     a.sign_words = P.desc.ld / 32;
@@ -751,7 +776,7 @@ hipError_t launch_segment_scales(const dqgan_plan_s &P, float eta, const float *
     }
     const int64_t n = static_cast<int64_t>(D.M) * D.n_seg;
     hipLaunchKernelGGL(k_finalize, dim3(static_cast<unsigned>((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, st, D.kind,
-                       D.norm, D.levels, P.d_partial, P.d_pmax, P.n_pieces, P.d_seg_piece, P.d_off, D.M, D.n_seg,
+                       D.norm, P.level_count, P.d_partial, P.d_pmax, P.n_pieces, P.d_seg_piece, P.d_off, D.M, D.n_seg,
                        scales_in, scale_out, P.d_consts);
     return hipGetLastError();
 }
@@ -774,6 +799,12 @@ hipError_t launch_encode(const dqgan_plan_s &P, float eta, uint32_t t, const flo
     else if (kind == kQsgd)
         hipLaunchKernelGGL((k_encode_rows<kQsgd, 4>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
                            P.d_consts, P.d_off, P.d_tile_seg, a);
+    else if (kind == kMbit && P.level_bits == 8)
+        hipLaunchKernelGGL((k_encode_rows<kMbit, 8>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
+    else if (kind == kMbit)
+        hipLaunchKernelGGL((k_encode_rows<kMbit, 4>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
+                           P.d_consts, P.d_off, P.d_tile_seg, a);
     else
         hipLaunchKernelGGL((k_encode_rows<kIdentity, 0>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
                            P.d_consts, P.d_off, P.d_tile_seg, a);
@@ -787,6 +818,8 @@ hipError_t launch_fused_dense(const dqgan_plan_s &P, float eta, uint32_t t, cons
     if (kind == kSign) return fused_by_m<kSign, 0>(P, a, G, E, W, WX, w, Qhat, st);
     if (kind == kQsgd && P.level_bits == 8) return fused_by_m<kQsgd, 8>(P, a, G, E, W, WX, w, Qhat, st);
     if (kind == kQsgd) return fused_by_m<kQsgd, 4>(P, a, G, E, W, WX, w, Qhat, st);
+    if (kind == kMbit && P.level_bits == 8) return fused_by_m<kMbit, 8>(P, a, G, E, W, WX, w, Qhat, st);
+    if (kind == kMbit) return fused_by_m<kMbit, 4>(P, a, G, E, W, WX, w, Qhat, st);
     return fused_by_m<kIdentity, 0>(P, a, G, E, W, WX, w, Qhat, st);
 }
 
@@ -794,11 +827,15 @@ hipError_t launch_pack(const dqgan_plan_s &P, const uint16_t *codes, const dqgan
     const RowArgs a = row_args(P, 0.0f, 0);
     const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
     if (P.desc.kind == kSign)
-        hipLaunchKernelGGL(k_pack<0>, grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+        hipLaunchKernelGGL((k_pack<0, kSign>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+    else if (P.desc.kind == kMbit && P.level_bits == 8)
+        hipLaunchKernelGGL((k_pack<8, kMbit>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+    else if (P.desc.kind == kMbit)
+        hipLaunchKernelGGL((k_pack<4, kMbit>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
     else if (P.level_bits == 8)
-        hipLaunchKernelGGL(k_pack<8>, grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+        hipLaunchKernelGGL((k_pack<8, kQsgd>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
     else
-        hipLaunchKernelGGL(k_pack<4>, grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
+        hipLaunchKernelGGL((k_pack<4, kQsgd>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
     return hipGetLastError();
 }
 
@@ -818,6 +855,12 @@ hipError_t launch_unpack_dense(const dqgan_plan_s &P, const dqgan_wire &w, float
                            P.d_off, P.d_tile_seg, a);
     else if (kind == kQsgd)
         hipLaunchKernelGGL((k_unpack<kQsgd, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
+                           P.d_off, P.d_tile_seg, a);
+    else if (kind == kMbit && P.level_bits == 8)
+        hipLaunchKernelGGL((k_unpack<kMbit, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
+                           P.d_off, P.d_tile_seg, a);
+    else if (kind == kMbit)
+        hipLaunchKernelGGL((k_unpack<kMbit, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
                            P.d_off, P.d_tile_seg, a);
     else
         hipLaunchKernelGGL((k_unpack<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat,
@@ -842,6 +885,12 @@ hipError_t launch_aggregate_dense(const dqgan_plan_s &P, const dqgan_wire &w, fl
                            P.d_consts, P.d_off, P.d_tile_seg, a, im);
     else if (kind == kQsgd)
         hipLaunchKernelGGL((k_aggregate<kQsgd, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    else if (kind == kMbit && P.level_bits == 8)
+        hipLaunchKernelGGL((k_aggregate<kMbit, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
+                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
+    else if (kind == kMbit)
+        hipLaunchKernelGGL((k_aggregate<kMbit, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
                            P.d_consts, P.d_off, P.d_tile_seg, a, im);
     else
         hipLaunchKernelGGL((k_aggregate<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,

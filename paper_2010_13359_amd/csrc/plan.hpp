@@ -68,7 +68,8 @@ struct dqgan_plan_s {
     dqgan_desc desc{};
     std::vector<int64_t> offsets;  // host copy, n_seg + 1
     int device = 0;
-    int level_bits = 0;            // QSGD: 8 (s = 255) or 4 (s = 15)
+    int level_bits = 0;            // QSGD: 8 (s = 255) or 4 (s = 15); MBIT: m
+    int level_count = 0;           // quantizer levels: QSGD s; MBIT k = 2^(m-1) - 1
     int64_t n_tiles = 0;           // ld / 1024
 
     int64_t *d_off = nullptr;       // [n_seg + 1]
@@ -84,7 +85,7 @@ struct dqgan_plan_s {
 
 namespace dq {
 
-// Dense compressors (SIGN, QSGD, IDENTITY).
+// Dense compressors (SIGN, QSGD, MBIT, IDENTITY).
 hipError_t launch_segment_scales(const dqgan_plan_s &P, float eta, const float *G, const float *E,
                                  const float *scales_in, float *scale_out, hipStream_t st);
 hipError_t launch_consts_from_scales(const dqgan_plan_s &P, const float *scales, hipStream_t st);

@@ -13,9 +13,9 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libdqgan.so")
 
-SIGN, QSGD, TOPK, IDENTITY = 0, 1, 2, 3
+SIGN, QSGD, TOPK, IDENTITY, MBIT = 0, 1, 2, 3, 4
 NORM_NONE, L1, L2, LINF = 0, 1, 2, 3
-KINDS = {"sign": SIGN, "qsgd": QSGD, "topk": TOPK, "identity": IDENTITY}
+KINDS = {"sign": SIGN, "qsgd": QSGD, "topk": TOPK, "identity": IDENTITY, "mbit": MBIT}
 NORMS = {"none": NORM_NONE, "l1": L1, "l2": L2, "linf": LINF}
 
 OK, EINVAL, EALIGN, ENOMEM, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
@@ -114,7 +114,7 @@ class Plan:
         self.ld = int(ld) if ld else (self.d + 1023) // 1024 * 1024
         self.kind = KINDS[kind] if isinstance(kind, str) else int(kind)
         if norm is None:
-            norm = {SIGN: "l1", QSGD: "l2"}.get(self.kind, "none")
+            norm = {SIGN: "l1", QSGD: "l2", MBIT: "linf"}.get(self.kind, "none")
         self.norm = NORMS[norm] if isinstance(norm, str) else int(norm)
         self.levels, self.k, self.seed = int(levels), int(k), int(seed)
         offs = list(seg_offsets) if seg_offsets is not None else [0, self.d]
@@ -128,7 +128,7 @@ class Plan:
 
     @classmethod
     def from_workload(cls, w):
-        return cls(w.d, w.M, w.kind, w.seg_offsets, w.norm if w.kind in ("sign", "qsgd") else "none",
+        return cls(w.d, w.M, w.kind, w.seg_offsets, w.norm if w.kind in ("sign", "qsgd", "mbit") else "none",
                    w.levels, w.k, w.quant_seed, w.ld)
 
     def close(self):

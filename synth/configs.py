@@ -133,10 +133,20 @@ def _build(index):
         sig = list(_log_uniform(rng2, 1e-4, 1e-1, len(sizes)))
         groups = [(off[j], off[j + 1]) for j in range(len(sizes))]
         return Workload(4, "large-generator", d, 64, "topk", "none", 0, d // 100, 1e-4, 5, off, groups, sig, "normal")
+    if index == 5:
+        # the paper's experimental setting: DCGAN with 8-bit codes and Hou et
+        # al.'s infinity-norm scale (Appendix A quantizer)
+        w = _build(2)
+        return Workload(5, "dcgan-hou8", w.d, w.M, "mbit", "linf", 8, 0, w.eta, w.T, w.seg_offsets, w.groups,
+                        w.group_scale, w.law)
+    if index == 6:
+        w = _build(3)
+        return Workload(6, "resnet-wgan-gp-hou8", w.d, w.M, "mbit", "linf", 8, 0, w.eta, w.T, w.seg_offsets,
+                        w.groups, w.group_scale, w.law)
     raise KeyError(index)
 
 
-CONFIGS = {i: None for i in range(5)}
+CONFIGS = {i: None for i in range(7)}
 
 
 def get(index) -> Workload:

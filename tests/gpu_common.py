@@ -99,8 +99,9 @@ def compare_step(w, gpu, ref, check_padding=True):
     assert_same("qhat", gpu["qhat"][:d], ref["qhat"][:d])
     if w.kind in ("sign", "qsgd"):
         assert_same("sign plane", gpu["sign"], ref["sign"])
+    if w.kind in ("sign", "qsgd", "mbit"):
         assert_same("scale", gpu["scale"], ref["scale"])
-    if w.kind == "qsgd":
+    if w.kind in ("qsgd", "mbit"):
         assert_same("level plane", gpu["level"], ref["level"])
     if w.kind == "topk":
         assert_same("idx", gpu["idx"], ref["idx"])

@@ -74,17 +74,22 @@ def test_c2_full_teacher_forced():
 
 
 @pytest.mark.timeout(300)
-def test_c3_sampled_segments():
+@pytest.mark.parametrize("index", [3, 6])
+def test_c3_c6_sampled_segments(index):
+    """C3: 4-bit quantizer, L2; C6: the same shape with the paper's 8-bit
+    sign-magnitude codes and the infinity-norm scale."""
     from oracle import oracle as orc
     import synth
-    w = synth.get(3)
-    print("C3 sampled", flush=True)
+    w = synth.get(index)
+    print("C%d sampled" % index, flush=True)
     plan, G, pre, E, W, WX, wire = _run(w)
     t = 2
     sizes = np.diff(w.seg_offsets)
     picks = sorted({int(np.argmin(sizes)), int(np.argsort(sizes)[len(sizes) // 2]), int(np.argmax(sizes))})
     scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
-    sign_rows = wire.sign.view(w.M, -1).cpu().numpy().view(np.uint32)
+    mbit = w.kind == "mbit"
+    k_levels = (1 << (w.levels - 1)) - 1 if mbit else w.levels
+    sign_rows = None if mbit else wire.sign.view(w.M, -1).cpu().numpy().view(np.uint32)
     level_rows = wire.level.view(w.M, -1).cpu().numpy().view(np.uint32)
     eta = np.float32(w.eta)
     for j in picks:
@@ -97,14 +102,18 @@ def test_c3_sampled_segments():
         enew = np.empty((w.M, n), np.float32)
         for m in range(w.M):
             p = orc.ef_accumulate(eta, Gs[m], Es[m])
-            own = orc.scale(p, "l2")
+            own = orc.scale(p, w.norm)
             assert abs(float(scales[m, j]) - float(own)) <= 1e-5 * float(own), (j, m)
-            bits, lv, ph, e = orc.qsgd_encode(p, scales[m, j], w.levels, w.quant_seed, m, t, i0=a)
+            bits, lv, ph, e = orc.qsgd_encode(p, scales[m, j], k_levels, w.quant_seed, m, t, i0=a)
             phat[m], enew[m] = ph, e
-            gs = orc.unpack_bits(sign_rows[m], 1, b)[a:b]
-            gl = orc.unpack_bits(level_rows[m], 4, b)[a:b]
-            assert_same("sign bits seg %d row %d" % (j, m), gs, bits.astype(np.uint16))
-            assert_same("levels seg %d row %d" % (j, m), gl, lv)
+            if mbit:
+                codes = orc.unpack_bits(level_rows[m], w.levels, b)[a:b]
+                assert_same("codes seg %d row %d" % (j, m), codes, orc.mbit_fields(bits, lv, w.levels))
+            else:
+                gs = orc.unpack_bits(sign_rows[m], 1, b)[a:b]
+                gl = orc.unpack_bits(level_rows[m], 4, b)[a:b]
+                assert_same("sign bits seg %d row %d" % (j, m), gs, bits.astype(np.uint16))
+                assert_same("levels seg %d row %d" % (j, m), gl, lv)
         assert_same("e_t seg %d" % j, E[:, a:b].cpu().numpy(), enew)
         q = orc.aggregate(phat, n)
         wt = orc.omd_update(q, Ws)

@@ -38,6 +38,13 @@ CASES = {
                                         eta=1e-2, seed=16),
     "sign_m33_masked": lambda: custom(d=4100, M=33, kind="sign", seg_offsets=[0, 64, 4100], eta=1e-2, seed=17),
     "qsgd15_m65_one_lane": lambda: custom(d=3000, M=65, kind="qsgd", levels=15, eta=1e-2, seed=18),
+    "mbit8_linf_m4": lambda: custom(d=5000, M=4, kind="mbit", levels=8, norm="linf", seg_offsets=[0, 1234, 5000],
+                                    eta=1e-2, seed=19),
+    "mbit8_linf_m32_many": lambda: custom(d=70001, M=32, kind="mbit", levels=8, norm="linf",
+                                          seg_offsets=[0, 64, 65, 1000, 4097, 30000, 65536, 70001], eta=1e-2, seed=20),
+    "mbit4_l2_m16": lambda: custom(d=20000, M=16, kind="mbit", levels=4, norm="l2", seg_offsets=[0, 7, 19999, 20000],
+                                   eta=1e-2, seed=21),
+    "mbit4_linf_m5_generic": lambda: custom(d=9000, M=5, kind="mbit", levels=4, norm="linf", eta=1e-2, seed=22),
     "identity_m2": lambda: custom(d=4097, M=2, kind="identity", eta=1e-2, seed=12),
     "identity_m1": lambda: custom(d=1500, M=1, kind="identity", eta=1e-2, seed=13),
 }
@@ -85,7 +92,7 @@ def test_unfused_equals_fused(name):
 
 
 @pytest.mark.parametrize("name", ["sign_2seg_m4", "qsgd15_l2_m4", "qsgd255_l2_m8", "qsgd15_l2_m32_many",
-                                  "identity_m2", "sign_tiny_segs_m2"])
+                                  "identity_m2", "sign_tiny_segs_m2", "mbit8_linf_m32_many", "mbit4_l2_m16"])
 def test_unpack_matches_oracle_decode(name):
     """The server's decode of the message (dqgan_unpack) equals the oracle's
     decode of the same message planes."""
@@ -105,6 +112,13 @@ def test_unpack_matches_oracle_decode(name):
     for m in range(w.M):
         if w.kind == "identity":
             exp = out["val"][m, :w.d]
+        elif w.kind == "mbit":
+            k = (1 << (w.levels - 1)) - 1
+            signs, levels = orc.mbit_split(orc.unpack_bits(out["level"][m], w.levels, w.d), w.levels)
+            exp = np.empty(w.d, np.float32)
+            for j in range(w.n_seg):
+                a0, a1 = w.seg_offsets[j], w.seg_offsets[j + 1]
+                exp[a0:a1] = orc.decode_segment("qsgd", signs[a0:a1], levels[a0:a1], out["scale"][m, j], k)
         else:
             signs = orc.unpack_bits(out["sign"][m], 1, w.d)
             levels = orc.unpack_bits(out["level"][m], b, w.d) if b else np.zeros(w.d, np.uint16)
@@ -116,13 +130,13 @@ def test_unpack_matches_oracle_decode(name):
         assert np.all(got[m, w.d:] == 0)
 
 
-@pytest.mark.parametrize("kind,levels", [("sign", 0), ("qsgd", 15), ("qsgd", 255)])
+@pytest.mark.parametrize("kind,levels", [("sign", 0), ("qsgd", 15), ("qsgd", 255), ("mbit", 8), ("mbit", 4)])
 def test_pack_matches_oracle(kind, levels):
     import torch
     from oracle import oracle as orc
     w = custom(d=10007, M=3, kind=kind, levels=levels, seg_offsets=[0, 5000, 10007], seed=14)
     rng = np.random.default_rng(1)
-    smax = levels if levels else 0
+    smax = ((1 << (levels - 1)) - 1) if kind == "mbit" else (levels if levels else 0)
     lv = rng.integers(0, smax + 1, (w.M, w.ld)).astype(np.uint16)
     sg = rng.integers(0, 2, (w.M, w.ld)).astype(np.uint16)
     codes = (sg << 15) | lv
@@ -137,6 +151,10 @@ def test_pack_matches_oracle(kind, levels):
     s.close()
     b = {255: 8, 15: 4}.get(levels, 0)
     for m in range(w.M):
+        if kind == "mbit":
+            codes = orc.mbit_fields(sg[m, :w.d].astype(np.uint8), lv[m, :w.d], levels)
+            assert_same("code words", out["level"][m], orc.pack_bits(codes, levels, w.ld * levels // 32))
+            continue
         exp_s = orc.pack_bits(sg[m, :w.d], 1, w.ld // 32)
         assert_same("sign words", out["sign"][m], exp_s)
         if b:
