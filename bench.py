@@ -65,15 +65,23 @@ def algorithmic_bytes(w):
     read and write e, write the evaluation point, write the message; per
     element read and write w; per (worker, segment) the scale."""
     per_mi = 16.0 + wire_bits(w) / 8.0
-    return w.M * w.d * per_mi + 8.0 * w.d + 4.0 * w.M * w.n_seg
+    scales = 4.0 * w.M * w.n_seg if w.kind in ("sign", "qsgd", "mbit") else 0.0
+    return w.M * w.d * per_mi + 8.0 * w.d + scales
 
 
 def workload_label(w):
-    comp = {"sign": "scaled sign (L1 mean)", "qsgd": "s-level quantizer s=%d %s" % (w.levels, w.norm.upper()),
-            "topk": "top-k k=%d" % w.k, "identity": "identity",
-            "mbit": "%d-bit sign-magnitude quantizer (k=%d) %s" % (w.levels, (1 << (w.levels - 1)) - 1,
-                                                                  w.norm.upper())}[w.kind]
-    return "C%d %s: d=%d, M=%d workers, %s, %d segments, eta=%g" % (w.index, w.name, w.d, w.M, comp, w.n_seg, w.eta)
+    if w.kind == "sign":
+        comp = "scaled sign (L1 mean)"
+    elif w.kind == "qsgd":
+        comp = "s-level quantizer s=%d %s" % (w.levels, w.norm.upper())
+    elif w.kind == "mbit":
+        comp = "%d-bit sign-magnitude quantizer (k=%d) %s" % (w.levels, (1 << (w.levels - 1)) - 1, w.norm.upper())
+    elif w.kind == "topk":
+        comp = "top-k k=%d" % w.k
+    else:
+        comp = "identity"
+    scope = "per row" if w.kind == "topk" else "%d segments" % w.n_seg
+    return "C%d %s: d=%d, M=%d workers, %s, %s, eta=%g" % (w.index, w.name, w.d, w.M, comp, scope, w.eta)
 
 
 def traffic_record(kernel_key, group):
