@@ -1,17 +1,21 @@
-// Kernels of the dense compressors: scaled sign, s-level stochastic
-// quantizer, identity (Algorithm 2 of arXiv:2010.13359 with the compressors
-// of its Section 2.4).
+// Element-major kernels of Algorithm 2 (arXiv:2010.13359): the statistics
+// pass of the segment-scaled compressors (scaled sign, s-level quantizer,
+// m-bit sign-magnitude quantizer), the fused apply pass of every compressor
+// (top-k included), and the separate pack / unpack / aggregate / OMD kernels.
 //
 // Passes over HBM per iteration:
 //   1. segment statistics: per (worker, segment) sum |p|, sum p^2 or max |p|
 //      of p = fl(fl(eta g) + e), one workgroup per piece, binary64 partials;
 //      a tiny kernel then combines the partials of each segment in piece
 //      order (deterministic) into the scale and the quantizer constants.
-//   2. the fused step: element-major; a lane owns one quad of 4 elements and
-//      walks the M workers in ascending order, encoding, writing e_t and the
-//      message, and summing p-hat in registers; then w_t = w_{t-1} - q-hat and
-//      the M evaluation points w_t - (fl(eta g) + e_t), whose right operands
-//      it kept in registers.
+//   2. the fused apply pass (k_fused_split): a workgroup covers 256 elements
+//      of all M workers, its waves splitting the workers; each lane encodes
+//      one quad of 4 elements per worker row, writes e_t and the message,
+//      keeps p-hat and fl(eta g) + e_t in registers; the ascending-worker sum
+//      is chained through LDS; the last wave of the chain applies
+//      w_t = w_{t-1} - q-hat; every wave then writes its rows' evaluation
+//      points w_t - (fl(eta g) + e_t).  k_fused (one lane walks all M rows)
+//      serves M > 64.
 #include "device.hpp"
 #include "plan.hpp"
 

@@ -11,12 +11,12 @@
 //     band [lo, hi];
 //  3. full pass: per 256-element tile the number of keys above hi, and every
 //     in-band (key, index) appended to a candidate list;
-//  4. exact radix select of the remaining rank among the candidates (six
-//     digits of the composite key) gives T and I;
+//  4. exact radix select of the remaining rank among the candidates (digits
+//     of key - lo, then of ~index when the k-th key is shared) gives T and I;
 //  5. the selected candidates are added to their tiles' counts.
 // If the band missed the k-th key (or the candidates overflow), the row falls
-// back to a full-row radix select over the same six digits (one read of the
-// row per digit) and a recount.  Finally an exclusive scan of the tile
+// back to a full-row radix select over six digits of (key, ~index) (one read
+// of the row per digit) and a recount.  Finally an exclusive scan of the tile
 // counts gives each tile's first output position, which the fused apply
 // pass uses to write (value, index) in ascending index order.
 #include "device.hpp"
