@@ -180,8 +180,12 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                       TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
                                                       uint2 *__restrict__ cand, int64_t cap) {
-    __shared__ uint2 buf[16 * kTopkTile];
-    __shared__ uint32_t nbuf, base, nab;
+    // Candidates are staged in a small LDS buffer (few per tile are in the
+    // band); a wave whose reservation does not fit appends straight to the
+    // row's list, and only the valid prefix [0, valid_end) is flushed.
+    constexpr uint32_t kStage = 1024;
+    __shared__ uint2 buf[kStage];
+    __shared__ uint32_t nbuf, base, nab, valid_end;
     const int m = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const uint32_t lo = rows[m].lo, hi = rows[m].hi;
@@ -190,9 +194,11 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     if (threadIdx.x == 0) {
         nbuf = 0;
         nab = 0;
+        valid_end = kStage;
     }
     __syncthreads();
     const uint64_t below = (uint64_t(1) << lane) - 1;
+    uint2 *crow = cand + static_cast<int64_t>(m) * cap;
     // The wave's four tiles are loaded before any of them is examined.
     f32x4 gvs[4], evs[4];
 #pragma unroll
@@ -234,24 +240,41 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                 uint32_t wbase = 0;
                 if (lane == 0) wbase = atomicAdd(&nbuf, tot);
                 wbase = __shfl(wbase, 0);
+                if (wbase + tot <= kStage) {
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    if ((cmask >> k) & 1u) {
-                        buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
-                        ++pre;
+                    for (int k = 0; k < 4; ++k) {
+                        if ((cmask >> k) & 1u) {
+                            buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                            ++pre;
+                        }
+                    }
+                } else {
+                    uint32_t gbase = 0;
+                    if (lane == 0) {
+                        atomicMin(&valid_end, wbase);
+                        gbase = atomicAdd(&rows[m].n_cand, tot);
+                    }
+                    gbase = __shfl(gbase, 0);
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        if ((cmask >> k) & 1u) {
+                            const int64_t pos = static_cast<int64_t>(gbase) + pre;
+                            if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                            ++pre;
+                        }
                     }
                 }
             }
         }
     }
     __syncthreads();
+    const uint32_t n_valid = nbuf < valid_end ? nbuf : valid_end;
     if (threadIdx.x == 0) {
-        base = nbuf ? atomicAdd(&rows[m].n_cand, nbuf) : 0u;
+        base = n_valid ? atomicAdd(&rows[m].n_cand, n_valid) : 0u;
         if (nab) atomicAdd(&rows[m].n_above, nab);
     }
     __syncthreads();
-    uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-    for (uint32_t j = threadIdx.x; j < nbuf; j += kBlock) {
+    for (uint32_t j = threadIdx.x; j < n_valid; j += kBlock) {
         const int64_t pos = static_cast<int64_t>(base) + j;
         if (pos < cap) crow[pos] = buf[j];
     }
