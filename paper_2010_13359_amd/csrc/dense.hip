@@ -106,7 +106,10 @@ __global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int lev
                                                      const int64_t *__restrict__ off, int32_t M, int32_t n_seg,
                                                      const float *__restrict__ scales_in, float *__restrict__ scale_out,
                                                      float2 *__restrict__ consts) {
-    const int64_t tid = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;
+    // One wave per (worker, segment): lane l adds the segment's pieces
+    // l, l+64, ... in order, then a fixed butterfly combines the lanes.
+    const int64_t tid = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) >> 6;
+    const int lane = threadIdx.x & 63;
     if (tid >= static_cast<int64_t>(M) * n_seg) return;
     const int m = static_cast<int>(tid / n_seg);
     const int j = static_cast<int>(tid % n_seg);
@@ -115,16 +118,23 @@ __global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int lev
         sc = scales_in[tid];
     } else if (norm == DQGAN_LINF) {
         float mx = 0.0f;
-        for (int p = seg_piece[j]; p < seg_piece[j + 1]; ++p) mx = fmaxf(mx, pmax[static_cast<int64_t>(m) * n_pieces + p]);
+        for (int p = seg_piece[j] + lane; p < seg_piece[j + 1]; p += 64)
+            mx = fmaxf(mx, pmax[static_cast<int64_t>(m) * n_pieces + p]);
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o));
         sc = mx;
     } else {
         double s = 0.0;
-        for (int p = seg_piece[j]; p < seg_piece[j + 1]; ++p) s += partial[static_cast<int64_t>(m) * n_pieces + p];
+        for (int p = seg_piece[j] + lane; p < seg_piece[j + 1]; p += 64)
+            s += partial[static_cast<int64_t>(m) * n_pieces + p];
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
         if (norm == DQGAN_L1)
             sc = static_cast<float>(s / static_cast<double>(off[j + 1] - off[j]));
         else
             sc = static_cast<float>(sqrt(s));
     }
+    if (lane != 0) return;
     if (scale_out) scale_out[tid] = sc;
     float2 c;
     if (kind == kQsgd || kind == kMbit) {
@@ -779,7 +789,8 @@ hipError_t launch_segment_scales(const dqgan_plan_s &P, float eta, const float *
         if (err != hipSuccess) return err;
     }
     const int64_t n = static_cast<int64_t>(D.M) * D.n_seg;
-    hipLaunchKernelGGL(k_finalize, dim3(static_cast<unsigned>((n + kBlock - 1) / kBlock)), dim3(kBlock), 0, st, D.kind,
+    // one wave per (worker, segment)
+    hipLaunchKernelGGL(k_finalize, dim3(static_cast<unsigned>((n * 64 + kBlock - 1) / kBlock)), dim3(kBlock), 0, st, D.kind,
                        D.norm, P.level_count, P.d_partial, P.d_pmax, P.n_pieces, P.d_seg_piece, P.d_off, D.M, D.n_seg,
                        scales_in, scale_out, P.d_consts);
     return hipGetLastError();
