@@ -13,8 +13,11 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-SRC = os.path.join(_HERE, "dqgan_oracle.c")
-LIB = os.path.join(_HERE, "libdqgan_oracle.so")
+# DQGAN_ORACLE_DIR names another directory holding a dqgan_oracle.c to build
+# and load instead (the planted-mistake test uses it for altered copies).
+_DIR = os.environ.get("DQGAN_ORACLE_DIR") or _HERE
+SRC = os.path.join(_DIR, "dqgan_oracle.c")
+LIB = os.path.join(_DIR, "libdqgan_oracle.so")
 CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
 
 KIND = {"sign": 0, "qsgd": 1, "topk": 2, "identity": 3, "mbit": 4}

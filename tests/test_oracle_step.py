@@ -32,6 +32,74 @@ def test_aggregate_order_golden(oracle_mod):
         assert out["qhat"][0] == np.float32(g[ex + "_qhat"][0])
 
 
+def test_aggregate_divides_once_golden(oracle_mod):
+    """M = 3: the average is the ascending sum divided once by M; the
+    hand-derived value differs from the sum times the rounded 1/M."""
+    g = load_golden("aggregate_mean_example.txt")
+    ph = np.array(g["c_phat"], np.float32).reshape(3, 1)
+    want = np.float32(g["c_qhat"][0])
+    assert want != np.float32(g["c_reciprocal_qhat"][0])
+    assert oracle_mod.aggregate(ph, 1)[0] == want
+    w = custom(d=1, M=3, kind="identity", eta=1.0, seed=0, ld=1024)
+    G = np.zeros((3, w.ld), np.float32)
+    G[:, 0] = ph[:, 0]
+    out = oracle_mod.step(w.as_dict(), np.float32(1.0), 1, G, np.zeros((3, w.ld), np.float32),
+                          np.zeros(w.ld, np.float32))
+    assert out["qhat"][0] == want
+
+
+def test_step_quantizer_uses_row_index_counter(oracle_mod):
+    """In the full iteration, element i of worker m (in whichever segment)
+    rounds with the uniform of counter (i, m, t), drawn here from the
+    pure-Python Philox reference (itself pinned to numpy's Philox), and the
+    level follows equation (qsgd)'s rule in binary32."""
+    from oracle import philox_ref
+    seed, t = (7 | (2 << 32)), 3
+    w = custom(d=300, M=2, kind="qsgd", levels=15, seg_offsets=[0, 100, 300], eta=1.0, seed=seed, ld=1024)
+    rng = np.random.default_rng(31)
+    G = np.zeros((2, w.ld), np.float32)
+    G[:, :300] = rng.standard_normal((2, 300)).astype(np.float32)
+    out = oracle_mod.step(w.as_dict(), np.float32(1.0), t, G, np.zeros((2, w.ld), np.float32),
+                          np.zeros(w.ld, np.float32))
+    s = np.float32(15)
+    for m in range(2):
+        words = out["level"][m]
+        for j, (lo, hi) in enumerate(((0, 100), (100, 300))):
+            inv = s / out["scale"][m, j]
+            for i in range(lo, hi):
+                lev = (int(words[i // 8]) >> (4 * (i % 8))) & 15   # 4-bit fields, low to high
+                r = np.float32(abs(G[m, i]) * inv)  # p = fl(fl(1 * g) + 0) = g
+                l = min(np.floor(r), s)
+                frac = np.float32(0) if l == s else np.float32(r - l)
+                u = philox_ref.uniform(seed, i, m, t)
+                assert lev == min(int(l) + (1 if u < frac else 0), 15), (m, i)
+
+
+@pytest.mark.parametrize("kind,norm,levels", [("sign", "l1", 0), ("qsgd", "l2", 15), ("qsgd", "linf", 15),
+                                              ("qsgd", "l2", 255), ("mbit", "linf", 8), ("mbit", "l2", 4)])
+def test_step_scales_follow_norm(oracle_mod, kind, norm, levels):
+    """Each segment's scale in the full iteration is the norm the compressor
+    names (equation qsgd's L2, the max norm of Section 2.4 / Appendix A, the
+    mean magnitude of the scaled sign), checked with numpy's norms: the max
+    exactly, the others to binary32 rounding of the binary64 value."""
+    w = custom(d=500, M=3, kind=kind, levels=levels, norm=norm, seg_offsets=[0, 37, 300, 500], eta=1.0, seed=5,
+               ld=1024)
+    rng = np.random.default_rng(41)
+    G = np.zeros((3, w.ld), np.float32)
+    G[:, :500] = (rng.standard_normal((3, 500)) * np.exp(rng.uniform(-4, 0, (3, 500)))).astype(np.float32)
+    out = oracle_mod.step(w.as_dict(), np.float32(1.0), 1, G, np.zeros((3, w.ld), np.float32),
+                          np.zeros(w.ld, np.float32))
+    for m in range(3):
+        for j, (lo, hi) in enumerate(((0, 37), (37, 300), (300, 500))):
+            p = G[m, lo:hi].astype(np.float64)  # p = fl(fl(1 * g) + 0) = g
+            if norm == "linf":
+                assert out["scale"][m, j] == np.float32(np.abs(p).max())
+            elif norm == "l2":
+                np.testing.assert_allclose(out["scale"][m, j], np.linalg.norm(p), rtol=1.2e-7)
+            else:
+                np.testing.assert_allclose(out["scale"][m, j], np.abs(p).mean(), rtol=1.2e-7)
+
+
 def test_ef_accumulate_two_roundings(oracle_mod):
     """Reading of Algorithm 2's p = eta F + e: two binary32 roundings (the
     product, then the sum), no fused multiply-add.  numpy's binary32 ufuncs
