@@ -10,7 +10,8 @@ region; two gradient batches alternate between steps.
 Prints one JSON line.  `value` is gradient GB/s = M * d * 4 bytes / step time.
 `roofline` is the dominant kernel (the apply pass) against the 8 TB/s HBM
 peak, with its algorithmic bytes per launch; `step_roofline` is the same for
-the whole step.  `cpu_baseline` is the oracle (single-threaded C) on a
+the whole step, plus the HBM bytes the rocprofv3 counters measured for the
+step's two main kernels (profiles/traffic.json) over the step time.  `cpu_baseline` is the oracle (single-threaded C) on a
 bounded sample of the same workload.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
@@ -204,6 +205,9 @@ def main():
     step_ach = b_alg / (ms_step * 1e-3) / 1e9
     kernel_key = "apply_C%d" % w.index
     traffic = traffic_record(kernel_key, "dense")  # the apply pass of every compressor is in dense.hip
+    # the statistics pass's main kernel: segment partials, or top-k's full pass
+    stats_traffic = traffic_record("stats_C%d" % w.index, "topk" if w.kind == "topk" else "dense")
+    step_counter = (traffic + stats_traffic) if (traffic and stats_traffic) else None
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
@@ -216,7 +220,12 @@ def main():
                      "algorithmic_bytes_per_launch": b_alg, "ms_per_launch": round(t_apply, 4)},
         "step_roofline": {"achieved": round(step_ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                           "frac": round(step_ach / HBM_PEAK_GBS, 4), "ms_scales_pass": round(t_scales, 4),
-                          "ms_apply_pass": round(t_apply, 4)},
+                          "ms_apply_pass": round(t_apply, 4),
+                          # HBM bytes the counters saw for the two main kernels of the step
+                          # (re-reads of the statistics pass included) per step time
+                          "counter_bytes": step_counter,
+                          "counter_frac": (round(step_counter / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+                                           if step_counter else None)},
         "hbm_pct_of_peak": round(100 * step_ach / HBM_PEAK_GBS, 2),
         "wall_s_timed": round(t_wall, 3),
     }
