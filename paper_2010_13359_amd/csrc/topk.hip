@@ -174,8 +174,12 @@ __global__ __launch_bounds__(64) void k_topk_band(const uint32_t *__restrict__ h
 }
 
 // 3. Full pass: per tile the count of keys above the band, and the in-band
-// candidates appended to the row's list.  A workgroup covers 16 tiles of one
-// row (4 waves x 4 tiles) and appends its candidates with one atomic.
+// candidates appended to the row's list.  A workgroup covers 64 tiles of one
+// row in four rounds (each: 4 waves x 4 tiles, loaded before any is examined)
+// and appends its candidates with one atomic; four rounds per workgroup
+// rather than one spread its fixed costs (row bounds, staging set-up, the
+// final atomic) over 16384 elements.
+constexpr int kPassRounds = 4;
 __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                       TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
@@ -199,68 +203,71 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     __syncthreads();
     const uint64_t below = (uint64_t(1) << lane) - 1;
     uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-    // The wave's four tiles are loaded before any of them is examined.
-    f32x4 gvs[4], evs[4];
+    for (int round = 0; round < kPassRounds; ++round) {
+        const int64_t tb = (static_cast<int64_t>(blockIdx.x) * kPassRounds + round) * 16;
+        // The wave's four tiles of this round are loaded before any is examined.
+        f32x4 gvs[4], evs[4];
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        const int64_t tile = static_cast<int64_t>(blockIdx.x) * 16 + it * 4 + wave;
-        if (tile < n_tiles) {
-            const int64_t i0 = tile * kTopkTile + 4 * lane;
-            gvs[it] = ld_stream(g + i0);
-            evs[it] = ld_stream(e + i0);
+        for (int it = 0; it < 4; ++it) {
+            const int64_t tile = tb + it * 4 + wave;
+            if (tile < n_tiles) {
+                const int64_t i0 = tile * kTopkTile + 4 * lane;
+                gvs[it] = ld_stream(g + i0);
+                evs[it] = ld_stream(e + i0);
+            }
         }
-    }
 #pragma unroll
-    for (int it = 0; it < 4; ++it) {
-        const int64_t tile = static_cast<int64_t>(blockIdx.x) * 16 + it * 4 + wave;
-        if (tile < n_tiles) {
-            const int64_t i0 = tile * kTopkTile + 4 * lane;
-            const f32x4 gv = gvs[it], ev = evs[it];
-            uint32_t keys[4];
-            uint32_t above_n = 0, cmask = 0;
+        for (int it = 0; it < 4; ++it) {
+            const int64_t tile = tb + it * 4 + wave;
+            if (tile < n_tiles) {
+                const int64_t i0 = tile * kTopkTile + 4 * lane;
+                const f32x4 gv = gvs[it], ev = evs[it];
+                uint32_t keys[4];
+                uint32_t above_n = 0, cmask = 0;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                keys[k] = key_of(elem(gv, k), elem(ev, k), eta);
-                const bool valid = i0 + k < d;
-                above_n += __popcll(__ballot(valid && keys[k] > hi));
-                cmask |= ((valid && keys[k] >= lo && keys[k] <= hi) ? 1u : 0u) << k;
-            }
-            if (lane == 0) {
-                tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
-                if (above_n) atomicAdd(&nab, above_n);
-            }
-            uint32_t pre = 0, tot = 0;
+                for (int k = 0; k < 4; ++k) {
+                    keys[k] = key_of(elem(gv, k), elem(ev, k), eta);
+                    const bool valid = i0 + k < d;
+                    above_n += __popcll(__ballot(valid && keys[k] > hi));
+                    cmask |= ((valid && keys[k] >= lo && keys[k] <= hi) ? 1u : 0u) << k;
+                }
+                if (lane == 0) {
+                    tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
+                    if (above_n) atomicAdd(&nab, above_n);
+                }
+                uint32_t pre = 0, tot = 0;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const uint64_t b = __ballot((cmask >> k) & 1u);
-                pre += __popcll(b & below);
-                tot += __popcll(b);
-            }
-            if (tot) {
-                uint32_t wbase = 0;
-                if (lane == 0) wbase = atomicAdd(&nbuf, tot);
-                wbase = __shfl(wbase, 0);
-                if (wbase + tot <= kStage) {
+                for (int k = 0; k < 4; ++k) {
+                    const uint64_t b = __ballot((cmask >> k) & 1u);
+                    pre += __popcll(b & below);
+                    tot += __popcll(b);
+                }
+                if (tot) {
+                    uint32_t wbase = 0;
+                    if (lane == 0) wbase = atomicAdd(&nbuf, tot);
+                    wbase = __shfl(wbase, 0);
+                    if (wbase + tot <= kStage) {
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        if ((cmask >> k) & 1u) {
-                            buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
-                            ++pre;
+                        for (int k = 0; k < 4; ++k) {
+                            if ((cmask >> k) & 1u) {
+                                buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                                ++pre;
+                            }
                         }
-                    }
-                } else {
-                    uint32_t gbase = 0;
-                    if (lane == 0) {
-                        atomicMin(&valid_end, wbase);
-                        gbase = atomicAdd(&rows[m].n_cand, tot);
-                    }
-                    gbase = __shfl(gbase, 0);
+                    } else {
+                        uint32_t gbase = 0;
+                        if (lane == 0) {
+                            atomicMin(&valid_end, wbase);
+                            gbase = atomicAdd(&rows[m].n_cand, tot);
+                        }
+                        gbase = __shfl(gbase, 0);
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        if ((cmask >> k) & 1u) {
-                            const int64_t pos = static_cast<int64_t>(gbase) + pre;
-                            if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
-                            ++pre;
+                        for (int k = 0; k < 4; ++k) {
+                            if ((cmask >> k) & 1u) {
+                                const int64_t pos = static_cast<int64_t>(gbase) + pre;
+                                if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                                ++pre;
+                            }
                         }
                     }
                 }
@@ -642,8 +649,9 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kBlock), 0, st, G, E, eta,
                        D.d, D.ld, S.n_chunks, S.hist);
     hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(64), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
-    hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + 15) / 16), M), dim3(kBlock), 0, st, G, E,
-                       eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
+    const int64_t per_block = 16 * kPassRounds;
+    hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + per_block - 1) / per_block), M),
+                       dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
     hipLaunchKernelGGL(k_topk_select, dim3(M), dim3(1024), 0, st, S.rows, S.cand, S.cap, D.k, S.hist);
     hipLaunchKernelGGL(k_topk_count, dim3(64, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, S.tile_cnt, S.n_tiles);
     for (int pass = 0; pass < 6; ++pass) {
