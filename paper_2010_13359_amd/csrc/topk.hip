@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
         valid_end = kStage;
     }
     __syncthreads();
-    const uint64_t below = (uint64_t(1) << lane) - 1;
+    const uint32_t span = hi - lo;
     uint2 *crow = cand + static_cast<int64_t>(m) * cap;
     for (int round = 0; round < kPassRounds; ++round) {
         const int64_t tb = (static_cast<int64_t>(blockIdx.x) * kPassRounds + round) * 16;
@@ -221,35 +221,37 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
             const int64_t tile = tb + it * 4 + wave;
             if (tile < n_tiles) {
                 const int64_t i0 = tile * kTopkTile + 4 * lane;
-                const f32x4 gv = gvs[it], ev = evs[it];
+                // Only the last tile of a row can hold elements at or beyond d.
+                const bool full = (tile + 1) * kTopkTile <= d;
                 uint32_t keys[4];
-                uint32_t above_n = 0, cmask = 0;
+                uint64_t cb[4];  // wave masks of the in-band candidates, per element of the quad
+                uint32_t above_n = 0, tot = 0;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    keys[k] = key_of(elem(gv, k), elem(ev, k), eta);
-                    const bool valid = i0 + k < d;
+                    keys[k] = key_of(elem(gvs[it], k), elem(evs[it], k), eta);
+                    const bool valid = full || i0 + k < d;
                     above_n += __popcll(__ballot(valid && keys[k] > hi));
-                    cmask |= ((valid && keys[k] >= lo && keys[k] <= hi) ? 1u : 0u) << k;
+                    cb[k] = __ballot(valid && keys[k] - lo <= span);  // lo <= key <= hi
+                    tot += __popcll(cb[k]);
                 }
                 if (lane == 0) {
                     tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
                     if (above_n) atomicAdd(&nab, above_n);
                 }
-                uint32_t pre = 0, tot = 0;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint64_t b = __ballot((cmask >> k) & 1u);
-                    pre += __popcll(b & below);
-                    tot += __popcll(b);
-                }
                 if (tot) {
+                    // this lane's first slot: the wave's candidates in lower lanes
+                    uint32_t pre = 0;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k)
+                        pre = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(cb[k] >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(cb[k]), pre));
                     uint32_t wbase = 0;
                     if (lane == 0) wbase = atomicAdd(&nbuf, tot);
-                    wbase = __shfl(wbase, 0);
+                    wbase = __builtin_amdgcn_readfirstlane(wbase);
                     if (wbase + tot <= kStage) {
 #pragma unroll
                         for (int k = 0; k < 4; ++k) {
-                            if ((cmask >> k) & 1u) {
+                            if ((cb[k] >> lane) & 1u) {
                                 buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
                                 ++pre;
                             }
@@ -260,10 +262,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                             atomicMin(&valid_end, wbase);
                             gbase = atomicAdd(&rows[m].n_cand, tot);
                         }
-                        gbase = __shfl(gbase, 0);
+                        gbase = __builtin_amdgcn_readfirstlane(gbase);
 #pragma unroll
                         for (int k = 0; k < 4; ++k) {
-                            if ((cmask >> k) & 1u) {
+                            if ((cb[k] >> lane) & 1u) {
                                 const int64_t pos = static_cast<int64_t>(gbase) + pre;
                                 if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
                                 ++pre;
