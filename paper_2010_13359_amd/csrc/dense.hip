@@ -751,15 +751,17 @@ hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
 }
 
 // Launch shape of the fused step: up to 16 waves per workgroup, each owning
-// R = ceil(M / 16) rows (measured on C3, M = 32: 16 waves x 2 rows beats 8 x 4
-// and 4 x 8); larger M uses the one-lane-per-quad kernel.
+// R rows.  Measured: M = 32, 16 waves x 2 rows beats 8 x 4 and 4 x 8; for
+// 9 <= M <= 16, 8 waves x 2 rows beats 16 x 1 by 10-13 % (twice the loads in
+// flight per lane); M <= 8 (cache-resident sizes) keeps one row per wave.
+// Larger M uses the one-lane-per-quad kernel.
 template <int KIND, int LB>
 hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                       const dqgan_wire &w, float *Qhat, hipStream_t st) {
     const int M = P.desc.M;
     if (M <= 4) return split_launch<KIND, LB, 1, 4>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 8) return split_launch<KIND, LB, 1, 8>(P, a, G, E, W, WX, w, Qhat, st);
-    if (M <= 16) return split_launch<KIND, LB, 1, 16>(P, a, G, E, W, WX, w, Qhat, st);
+    if (M <= 16) return split_launch<KIND, LB, 2, 8>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 32) return split_launch<KIND, LB, 2, 16>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 64) return split_launch<KIND, LB, 4, 16>(P, a, G, E, W, WX, w, Qhat, st);
     if constexpr (KIND == kTopk) {

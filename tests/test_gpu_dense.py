@@ -37,6 +37,13 @@ CASES = {
     "qsgd15_m17_masked": lambda: custom(d=6000, M=17, kind="qsgd", levels=15, seg_offsets=[0, 2999, 6000],
                                         eta=1e-2, seed=16),
     "sign_m33_masked": lambda: custom(d=4100, M=33, kind="sign", seg_offsets=[0, 64, 4100], eta=1e-2, seed=17),
+    # 8 waves x 2 rows: an odd worker count leaves the last wave half empty and
+    # the waves beyond it idle
+    "qsgd255_m9_masked": lambda: custom(d=5000, M=9, kind="qsgd", levels=255, seg_offsets=[0, 1000, 5000],
+                                        eta=1e-2, seed=23),
+    "mbit8_m13_masked": lambda: custom(d=3333, M=13, kind="mbit", levels=8, norm="linf", seg_offsets=[0, 3333],
+                                       eta=1e-2, seed=24),
+    "topk_m11_masked": lambda: custom(d=7000, M=11, kind="topk", k=300, eta=1e-2, seed=25),
     "qsgd15_m65_one_lane": lambda: custom(d=3000, M=65, kind="qsgd", levels=15, eta=1e-2, seed=18),
     "mbit8_linf_m4": lambda: custom(d=5000, M=4, kind="mbit", levels=8, norm="linf", seg_offsets=[0, 1234, 5000],
                                     eta=1e-2, seed=19),
