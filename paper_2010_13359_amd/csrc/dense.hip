@@ -751,10 +751,11 @@ hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
 }
 
 // Launch shape of the fused step: up to 16 waves per workgroup, each owning
-// R rows.  Measured: M = 32, 16 waves x 2 rows beats 8 x 4 and 4 x 8; for
-// 9 <= M <= 16, 8 waves x 2 rows beats 16 x 1 by 10-13 % (twice the loads in
-// flight per lane); M <= 8 (cache-resident sizes) keeps one row per wave.
-// Larger M uses the one-lane-per-quad kernel.
+// R rows; more rows per wave means more loads in flight per lane.  Measured:
+// for 9 <= M <= 16, 8 waves x 2 rows beats 16 x 1 by 10-13 %; for
+// 17 <= M <= 32, 8 waves x 4 rows beats 16 x 2 by 2-3 % although it runs 6
+// rather than 8 waves per SIMD; M <= 8 (cache-resident sizes) keeps one row
+// per wave.  Larger M uses the one-lane-per-quad kernel.
 template <int KIND, int LB>
 hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                       const dqgan_wire &w, float *Qhat, hipStream_t st) {
@@ -762,7 +763,7 @@ hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, f
     if (M <= 4) return split_launch<KIND, LB, 1, 4>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 8) return split_launch<KIND, LB, 1, 8>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 16) return split_launch<KIND, LB, 2, 8>(P, a, G, E, W, WX, w, Qhat, st);
-    if (M <= 32) return split_launch<KIND, LB, 2, 16>(P, a, G, E, W, WX, w, Qhat, st);
+    if (M <= 32) return split_launch<KIND, LB, 4, 8>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 64) return split_launch<KIND, LB, 4, 16>(P, a, G, E, W, WX, w, Qhat, st);
     if constexpr (KIND == kTopk) {
         return hipErrorNotSupported;  // top-k plans are limited to M <= 64
