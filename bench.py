@@ -14,7 +14,7 @@ the whole step, plus the HBM bytes the rocprofv3 counters measured for the
 step's two main kernels (profiles/traffic.json) over the step time.  `cpu_baseline` is the oracle (single-threaded C) on a
 bounded sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--graph]
 """
 import argparse
 import hashlib
@@ -139,6 +139,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a plain device copy of 1 GiB (counter calibration)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the timed iterations in one HIP graph and time its replay (launch-bound sizes); "
+                         "the per-pass times then come from an eager run of the same iterations")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
@@ -184,15 +187,29 @@ def main():
         del a, b
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    graph = None
+    if args.graph:
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for k in range(args.steps):
+                one(args.warmup + 1 + k)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record()
-    for k in range(args.steps):
-        one(args.warmup + 1 + k, evs[k])
+    if graph is not None:
+        graph.replay()
+    else:
+        for k in range(args.steps):
+            one(args.warmup + 1 + k, evs[k])
     stop.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(stop)
+    if graph is not None:
+        # per-pass times: the same iterations again, eagerly, with events
+        for k in range(args.steps):
+            one(args.warmup + 1 + k, evs[k])
+        torch.cuda.synchronize()
     scales_ms = [e[0].elapsed_time(e[1]) for e in evs]
     apply_ms = [e[1].elapsed_time(e[2]) for e in evs]
     ms_step = total_ms / args.steps
@@ -213,7 +230,8 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": workload_label(w), "d": w.d, "M": w.M, "compressor": w.kind, "levels": w.levels,
-                   "k": w.k, "segments": w.n_seg, "parallelism": "single GPU; M workers as rows"},
+                   "k": w.k, "segments": w.n_seg, "parallelism": "single GPU; M workers as rows",
+                   "launch": "hip graph of the timed iterations" if args.graph else "eager"},
         "roofline": {"bound": "hbm", "kernel": "dqgan_step_apply (fused encode+EF+aggregate+OMD pass)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
@@ -229,6 +247,22 @@ def main():
         "hbm_pct_of_peak": round(100 * step_ach / HBM_PEAK_GBS, 2),
         "wall_s_timed": round(t_wall, 3),
     }
+    # Reference stream in the same process and on the same buffers (the
+    # reachable HBM rate of mixed read/write streams differs between
+    # allocations and boxes by up to 20 %): out = g + e, 2 reads + 1 write.
+    ref_ms = []
+    for _ in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        torch.add(Gs[0], E, out=WX)
+        b.record()
+        torch.cuda.synchronize()
+        ref_ms.append(a.elapsed_time(b))
+    ref_t = sorted(ref_ms)[1]
+    out["reference_stream"] = {"op": "torch.add(g, e, out=WX) over the step's own [M][ld] buffers (2 reads, 1 write)",
+                               "GB/s": round(3 * 4.0 * w.M * w.ld / (ref_t * 1e-3) / 1e9, 1),
+                               "ms": round(ref_t, 4)}
+    del graph
     plan.close()
     del Gs, E, W, WX, wire
     torch.cuda.empty_cache()
