@@ -34,7 +34,10 @@
  *    nothing.  A failed launch returns DQGAN_EHIP; faults of enqueued work
  *    surface at the caller's next synchronization.  No call aborts the
  *    process.  Only dqgan_plan_create and dqgan_plan_destroy allocate or free
- *    device memory.
+ *    device memory.  The per-iteration calls enqueue kernels only (plus, in
+ *    dqgan_pack, one device-to-device copy of the scales): no memset, no host
+ *    synchronization, so a caller may capture them in a HIP graph and replay
+ *    it.
  *  - A plan is bound to the device that was current at its creation; calls
  *    must be made with that device current.  A plan is not thread-safe, and
  *    two calls on one plan must not run concurrently on different streams
@@ -94,7 +97,7 @@ typedef struct {
     int32_t reserved;             /* must be 0                                      */
     int64_t k;                    /* TOPK: 1 <= k <= d, d < 2^32, M <= 64
                                      (larger M: DQGAN_EUNSUPPORTED)                 */
-    uint64_t seed;                /* QSGD: key of the Philox4x32-10 generator       */
+    uint64_t seed;                /* QSGD, MBIT: key of the Philox4x32-10 generator */
 } dqgan_desc;
 
 typedef struct dqgan_plan_s *dqgan_plan;
@@ -140,7 +143,7 @@ dqgan_status dqgan_wire_bytes(dqgan_plan plan, size_t *sign, size_t *level, size
  * pack, EF residual): p = fl(fl(eta*g) + e); p-hat = Q(p); e <- fl(p - p-hat);
  * the message goes to `out`.
  *   G:  [M][ld] gradients g_t (read).     E: [M][ld] e_{t-1} in, e_t out.
- *   t:  iteration number (QSGD: Philox counter word 2).
+ *   t:  iteration number (QSGD, MBIT: Philox counter word 2).
  *   scales_in: NULL to compute the segment scales from p (Section 2.4 /
  *     equation qsgd); else device fp32 [M][n_seg] scales to use instead
  *     (they are also copied to out->scale).  Ignored by TOPK and IDENTITY.
