@@ -15,7 +15,7 @@
 //      is chained through LDS; the last wave of the chain applies
 //      w_t = w_{t-1} - q-hat; every wave then writes its rows' evaluation
 //      points w_t - (fl(eta g) + e_t).  k_fused (one lane walks all M rows)
-//      serves M > 64.
+//      serves M > 128.
 #include "device.hpp"
 #include "plan.hpp"
 
@@ -736,6 +736,7 @@ hipError_t fused_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
 template <int KIND, int LB, int R, int NG>
 hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                         const dqgan_wire &w, float *Qhat, hipStream_t st) {
+    if (P.desc.M > R * NG) return hipErrorInvalidValue;  // every worker must belong to a wave
     TopkArgs ta{};
     if (KIND == kTopk) {
         ta.rows = P.topk.rows;
@@ -755,7 +756,10 @@ hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
 // for 9 <= M <= 16, 8 waves x 2 rows beats 16 x 1 by 10-13 %; for
 // 17 <= M <= 32, 8 waves x 4 rows beats 16 x 2 by 2-3 % although it runs 6
 // rather than 8 waves per SIMD; M <= 8 (cache-resident sizes) keeps one row
-// per wave.  Larger M uses the one-lane-per-quad kernel.
+// per wave; for 65 <= M <= 128, 16 waves x 8 rows (4 waves per SIMD) is a
+// third faster than the one-lane kernel.  Beyond 128 rows no register-resident
+// split fits (16 rows per lane need more than the 128 VGPRs a 16-wave
+// workgroup allows), and the one-lane-per-quad kernel serves.
 template <int KIND, int LB>
 hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                       const dqgan_wire &w, float *Qhat, hipStream_t st) {
@@ -768,6 +772,7 @@ hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, f
     if constexpr (KIND == kTopk) {
         return hipErrorNotSupported;  // top-k plans are limited to M <= 64
     } else {
+        if (M <= 128) return split_launch<KIND, LB, 8, 16>(P, a, G, E, W, WX, w, Qhat, st);
         return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
     }
 }

@@ -44,7 +44,11 @@ CASES = {
     "mbit8_m13_masked": lambda: custom(d=3333, M=13, kind="mbit", levels=8, norm="linf", seg_offsets=[0, 3333],
                                        eta=1e-2, seed=24),
     "topk_m11_masked": lambda: custom(d=7000, M=11, kind="topk", k=300, eta=1e-2, seed=25),
-    "qsgd15_m65_one_lane": lambda: custom(d=3000, M=65, kind="qsgd", levels=15, eta=1e-2, seed=18),
+    "qsgd15_m65_split8": lambda: custom(d=3000, M=65, kind="qsgd", levels=15, eta=1e-2, seed=18),
+    "sign_m128_split8": lambda: custom(d=2100, M=128, kind="sign", seg_offsets=[0, 100, 2100], eta=1e-2, seed=26),
+    "mbit4_m100_split8": lambda: custom(d=1500, M=100, kind="mbit", levels=4, norm="linf", eta=1e-2, seed=27),
+    "qsgd255_m130_one_lane": lambda: custom(d=1800, M=130, kind="qsgd", levels=255, seg_offsets=[0, 901, 1800],
+                                            eta=1e-2, seed=28),
     "mbit8_linf_m4": lambda: custom(d=5000, M=4, kind="mbit", levels=8, norm="linf", seg_offsets=[0, 1234, 5000],
                                     eta=1e-2, seed=19),
     "mbit8_linf_m32_many": lambda: custom(d=70001, M=32, kind="mbit", levels=8, norm="linf",

@@ -1,6 +1,6 @@
 """Seeded random shapes through the C ABI against the oracle (teacher-forced,
-bit-exact): every compressor, worker counts 1..70 (both fused-kernel
-families), lengths 1..60000 with ragged tails, random segment layouts down to
+bit-exact): every compressor, worker counts 1..140 (every launch shape of the fused
+kernel), lengths 1..60000 with ragged tails, random segment layouts down to
 one-element segments, random step sizes and residual magnitudes."""
 import numpy as np
 import pytest
@@ -20,7 +20,7 @@ def _random_case(seed):
     kind, extra = KINDS[seed % len(KINDS)]
     extra = dict(extra)
     d = int(rng.integers(1, 60001)) if seed % 3 else int(rng.integers(1, 300))
-    M = int(rng.choice([1, 2, 3, 4, 7, 8, 16, 17, 31, 32, 33, 64, 70]))
+    M = int(rng.choice([1, 2, 3, 4, 7, 8, 16, 17, 31, 32, 33, 64, 70, 100, 140]))
     if kind == "topk":
         M = min(M, 64)
         extra["k"] = int(rng.integers(1, d + 1)) if seed % 4 else max(1, d // 100)
