@@ -121,18 +121,24 @@ __device__ bool wave_find_desc(const uint32_t *h, int nb, uint32_t rank, uint32_
 }
 
 // 1. Sample histogram of key >> 16 (one 256-element chunk per 65536 elements).
-__global__ __launch_bounds__(kBlock) void k_topk_sample(const float *__restrict__ G, const float *__restrict__ E,
-                                                        float eta, int64_t d, int64_t ld, int64_t n_chunks,
-                                                        uint32_t *__restrict__ hist) {
+// The 128 KiB LDS histogram allows one workgroup per CU, so the workgroup
+// has 16 waves (each loads a chunk) to keep enough scattered loads in flight.
+constexpr int kSampleThreads = 1024;
+
+__global__ __launch_bounds__(kSampleThreads) void k_topk_sample(const float *__restrict__ G,
+                                                                const float *__restrict__ E, float eta, int64_t d,
+                                                                int64_t ld, int64_t n_chunks,
+                                                                uint32_t *__restrict__ hist) {
+    constexpr int kWaves = kSampleThreads / 64;
     __shared__ uint32_t h[kSampleBins];
     const int m = blockIdx.y;
-    for (int b = threadIdx.x; b < kSampleBins; b += kBlock) h[b] = 0;
+    for (int b = threadIdx.x; b < kSampleBins; b += kSampleThreads) h[b] = 0;
     __syncthreads();
     const float *g = G + static_cast<int64_t>(m) * ld;
     const float *e = E + static_cast<int64_t>(m) * ld;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int64_t c = static_cast<int64_t>(blockIdx.x) * 4 + wave; c < n_chunks;
-         c += static_cast<int64_t>(gridDim.x) * 4) {
+    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWaves + wave; c < n_chunks;
+         c += static_cast<int64_t>(gridDim.x) * kWaves) {
         const int64_t i0 = c * kSampleStride + 4 * lane;
         if (i0 < d) {
             const f32x4 gv = ld4(g + i0), ev = ld4(e + i0);
@@ -143,11 +149,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_sample(const float *__restrict_
     }
     __syncthreads();
     uint32_t *hm = hist + static_cast<int64_t>(m) * kSampleBins;
-    for (int b = threadIdx.x; b < kSampleBins; b += kBlock)
+    for (int b = threadIdx.x; b < kSampleBins; b += kSampleThreads)
         if (h[b]) atomicAdd(&hm[b], h[b]);
 }
 
-// 2. Candidate band of each row from its sample histogram.
 __global__ __launch_bounds__(64) void k_topk_band(const uint32_t *__restrict__ hist, TopkRow *__restrict__ rows,
                                                   uint32_t n_samples, int64_t d, int64_t k) {
     const int m = blockIdx.x;
@@ -647,9 +652,9 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     const unsigned M = static_cast<unsigned>(D.M);
     const int64_t nh = static_cast<int64_t>(D.M) * kSampleBins;
     hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(nh, 1024)), dim3(kBlock), 0, st, S.hist, nh, 0u);
-    const int64_t sb = (S.n_chunks + 3) / 4;
-    hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kBlock), 0, st, G, E, eta,
-                       D.d, D.ld, S.n_chunks, S.hist);
+    const int64_t sb = (S.n_chunks + kSampleThreads / 64 - 1) / (kSampleThreads / 64);
+    hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kSampleThreads), 0, st,
+                       G, E, eta, D.d, D.ld, S.n_chunks, S.hist);
     hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(64), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
     const int64_t per_block = 16 * kPassRounds;
     hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + per_block - 1) / per_block), M),
