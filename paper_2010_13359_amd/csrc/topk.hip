@@ -153,28 +153,91 @@ __global__ __launch_bounds__(kSampleThreads) void k_topk_sample(const float *__r
         if (h[b]) atomicAdd(&hm[b], h[b]);
 }
 
-__global__ __launch_bounds__(64) void k_topk_band(const uint32_t *__restrict__ hist, TopkRow *__restrict__ rows,
-                                                  uint32_t n_samples, int64_t d, int64_t k) {
+// Exclusive prefix sum of v over the 1024 threads of a workgroup (wsum: 16
+// words of LDS); total receives the sum over all threads.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *wsum, uint32_t &total) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint32_t incl = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_up(incl, o);
+        if (lane >= o) incl += x;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t wbase = 0, tot = 0;
+    for (int w = 0; w < 16; ++w) {
+        if (w < wave) wbase += wsum[w];
+        tot += wsum[w];
+    }
+    total = tot;
+    return wbase + incl - v;
+}
+
+// 2. Band: the sample ranks k/d * s -+ 8 sigma (binomial) bracket the k-th
+// key; the bins where the count from the top reaches them bound [lo, hi].
+__global__ __launch_bounds__(1024) void k_topk_band(const uint32_t *__restrict__ hist, TopkRow *__restrict__ rows,
+                                                    uint32_t n_samples, int64_t d, int64_t k) {
+    // thread t holds the t-th group of kPer bins counted from the top; a
+    // block scan finds the group where the count from the top reaches a
+    // rank, and that thread finds the bin in its registers.
+    constexpr int kPer = kSampleBins / 1024;
+    __shared__ uint32_t wsum[16];
+    __shared__ uint32_t found[2];
     const int m = blockIdx.x;
+    const int t = threadIdx.x;
     const uint32_t *h = hist + static_cast<int64_t>(m) * kSampleBins;
+    uint32_t asc[kPer];  // bins kSampleBins - kPer (t+1) .. kSampleBins - kPer t - 1, ascending
+    const uint4 *src = reinterpret_cast<const uint4 *>(h + kSampleBins - kPer * (t + 1));
+#pragma unroll
+    for (int q = 0; q < kPer / 4; ++q) {
+        const uint4 v = src[q];
+        asc[4 * q] = v.x;
+        asc[4 * q + 1] = v.y;
+        asc[4 * q + 2] = v.z;
+        asc[4 * q + 3] = v.w;
+    }
+    uint32_t s = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) s += asc[j];
+    if (t == 0) found[0] = found[1] = 0xFFFFFFFFu;
+    uint32_t total;
+    const uint32_t excl = block_exclusive_scan(s, wsum, total);  // count above this group
     const double f = static_cast<double>(k) / static_cast<double>(d);
-    const double s = static_cast<double>(n_samples);
-    const double mean = f * s;
-    const double sd = sqrt(s * f * (1.0 - f)) + 1.0;
+    const double ns = static_cast<double>(n_samples);
+    const double mean = f * ns;
+    const double sd = sqrt(ns * f * (1.0 - f)) + 1.0;
     const double z = 8.0;
-    uint32_t hi = 0x7FFFFFFFu, lo = 0u;
     const double a = floor(mean - z * sd);
-    uint32_t bin, above;
-    if (a >= 1.0 && wave_find_desc(h, kSampleBins, static_cast<uint32_t>(a) + 1u, bin, above))
-        hi = ((bin + 1u) << 16) - 1u;
     const double c = ceil(mean + z * sd);
-    if (c <= s && wave_find_desc(h, kSampleBins, static_cast<uint32_t>(c), bin, above)) lo = bin << 16;
-    if (lo > hi) lo = 0u;
-    if (threadIdx.x == 0) {
-        TopkRow r{};
-        r.lo = lo;
-        r.hi = hi;
-        rows[m] = r;
+    // ranks (from the top) whose bins bound the band: a + 1 for hi, c for lo
+    const uint32_t want[2] = {a >= 1.0 ? static_cast<uint32_t>(a) + 1u : 0u,
+                              c <= ns ? static_cast<uint32_t>(c) : 0u};
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+        const uint32_t rank = want[r];
+        if (rank != 0u && excl < rank && rank <= excl + s) {
+            uint32_t acc = excl;
+            for (int j = 0; j < kPer; ++j) {
+                const uint32_t cnt = asc[kPer - 1 - j];
+                if (acc + cnt >= rank) {
+                    found[r] = static_cast<uint32_t>(kSampleBins - 1 - (kPer * t + j));
+                    break;
+                }
+                acc += cnt;
+            }
+        }
+    }
+    __syncthreads();
+    if (t == 0) {
+        uint32_t hi = 0x7FFFFFFFu, lo = 0u;
+        if (found[0] != 0xFFFFFFFFu) hi = ((found[0] + 1u) << 16) - 1u;
+        if (found[1] != 0xFFFFFFFFu) lo = found[1] << 16;
+        if (lo > hi) lo = 0u;
+        TopkRow row{};
+        row.lo = lo;
+        row.hi = hi;
+        rows[m] = row;
     }
 }
 
@@ -508,24 +571,6 @@ __global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restr
 // chunks of the row.
 constexpr int kScanChunk = 4096;
 
-__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *wsum, uint32_t &total) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    uint32_t incl = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t x = __shfl_up(incl, o);
-        if (lane >= o) incl += x;
-    }
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    uint32_t wbase = 0, tot = 0;
-    for (int w = 0; w < 16; ++w) {
-        if (w < wave) wbase += wsum[w];
-        tot += wsum[w];
-    }
-    total = tot;
-    return wbase + incl - v;
-}
 
 __global__ __launch_bounds__(1024) void k_topk_scan_local(const uint32_t *__restrict__ tile_cnt,
                                                           uint32_t *__restrict__ tile_off,
@@ -655,7 +700,7 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     const int64_t sb = (S.n_chunks + kSampleThreads / 64 - 1) / (kSampleThreads / 64);
     hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kSampleThreads), 0, st,
                        G, E, eta, D.d, D.ld, S.n_chunks, S.hist);
-    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(64), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
+    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
     const int64_t per_block = 16 * kPassRounds;
     hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + per_block - 1) / per_block), M),
                        dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
