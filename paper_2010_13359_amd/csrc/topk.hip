@@ -362,6 +362,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
 // lie in [lo, hi]: the digits are taken over key - lo, 11 bits at a time from
 // the top of its width, then (only if the k-th key is shared and not every
 // tie is taken) over ~index.
+constexpr int kSelU = 8;  // candidates in flight per thread in the selection passes
+
 __global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows, const uint2 *__restrict__ cand,
                                                       int64_t cap, int64_t k, uint32_t *__restrict__ hist) {
     __shared__ uint32_t h[kDigitBins];
@@ -400,10 +402,20 @@ __global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows
         const int nb = 1 << wbits;
         for (int b = tid; b < nb; b += 1024) h[b] = 0u;
         __syncthreads();
-        for (uint32_t j = tid; j < n_cand; j += 1024) {
-            const uint32_t rel = crow[j].x - lo;
-            const bool play = top >= 32 || (rel >> top) == (kp >> top);
-            if (play) atomicAdd(&h[(rel >> shift) & dmask], 1u);
+        // kSelU candidates per thread per trip, all loads issued before use
+        for (uint64_t j0 = tid; j0 < n_cand; j0 += 1024 * kSelU) {
+            uint32_t keys[kSelU];
+#pragma unroll
+            for (int u = 0; u < kSelU; ++u) {
+                const uint64_t j = j0 + 1024u * u;
+                keys[u] = j < n_cand ? crow[j].x : 0u;
+            }
+#pragma unroll
+            for (int u = 0; u < kSelU; ++u) {
+                const uint32_t rel = keys[u] - lo;
+                const bool play = j0 + 1024u * u < n_cand && (top >= 32 || (rel >> top) == (kp >> top));
+                if (play) atomicAdd(&h[(rel >> shift) & dmask], 1u);
+            }
         }
         __syncthreads();
         if (tid < 64) {
@@ -430,10 +442,19 @@ __global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows
             const int nb = bins_of(pass);
             for (int b = tid; b < nb; b += 1024) h[b] = 0u;
             __syncthreads();
-            for (uint32_t j = tid; j < n_cand; j += 1024) {
-                const uint2 c = crow[j];
-                const uint32_t ni = ~c.y;
-                if (in_play(pass, c.x, ni, T, ip)) atomicAdd(&h[digit_of(pass, c.x, ni)], 1u);
+            for (uint64_t j0 = tid; j0 < n_cand; j0 += 1024 * kSelU) {
+                uint2 cs[kSelU];
+#pragma unroll
+                for (int u = 0; u < kSelU; ++u) {
+                    const uint64_t j = j0 + 1024u * u;
+                    cs[u] = j < n_cand ? crow[j] : make_uint2(0u, 0u);
+                }
+#pragma unroll
+                for (int u = 0; u < kSelU; ++u) {
+                    const uint32_t ni = ~cs[u].y;
+                    if (j0 + 1024u * u < n_cand && in_play(pass, cs[u].x, ni, T, ip))
+                        atomicAdd(&h[digit_of(pass, cs[u].x, ni)], 1u);
+                }
             }
             __syncthreads();
             if (tid < 64) {
@@ -466,11 +487,21 @@ __global__ __launch_bounds__(kBlock) void k_topk_count(const TopkRow *__restrict
     if (r.fallback) return;
     const uint32_t n = r.n_cand;
     const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n;
-         j += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const uint2 c = crow[j];
-        if (c.x > r.T || (c.x == r.T && c.y <= r.I))
-            atomicAdd(&tile_cnt[static_cast<int64_t>(m) * n_tiles + (c.y >> 8)], 1u);
+    uint32_t *trow = tile_cnt + static_cast<int64_t>(m) * n_tiles;
+    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock;
+    // kSelU candidates per thread per trip, all loads issued before use
+    for (int64_t j0 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j0 < n; j0 += step * kSelU) {
+        uint2 cs[kSelU];
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) {
+            const int64_t j = j0 + step * u;
+            cs[u] = j < n ? crow[j] : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) {
+            const uint2 c = cs[u];
+            if (j0 + step * u < n && (c.x > r.T || (c.x == r.T && c.y <= r.I))) atomicAdd(&trow[c.y >> 8], 1u);
+        }
     }
 }
 
