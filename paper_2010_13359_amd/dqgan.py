@@ -88,15 +88,29 @@ def _check(fn, status):
         raise DqganError(fn, status)
 
 
-def _ptr(t):
+F32 = (torch.float32,)
+U32 = (torch.int32, torch.uint32)    # bit patterns of uint32 words
+U16 = (torch.int16, torch.uint16)    # per-element codes of dqgan_pack
+
+
+def _ptr(t, name="tensor", nbytes=0, dtypes=None, device=None):
+    """Device pointer of `t` after the checks the C ABI cannot make: a
+    contiguous device tensor of the expected dtype, on the plan's device,
+    holding at least `nbytes` bytes.  None passes as NULL."""
     if t is None:
         return None
     if not isinstance(t, torch.Tensor):
-        raise TypeError("expected a torch.Tensor")
+        raise TypeError("%s: expected a torch.Tensor" % name)
     if not t.is_cuda:
-        raise ValueError("tensor must be in device memory")
+        raise ValueError("%s: tensor must be in device memory" % name)
     if not t.is_contiguous():
-        raise ValueError("tensor must be contiguous")
+        raise ValueError("%s: tensor must be contiguous" % name)
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError("%s: dtype %s, expected %s" % (name, t.dtype, " or ".join(str(d) for d in dtypes)))
+    if device is not None and t.device.index != device:
+        raise ValueError("%s: on cuda:%s, the plan is on cuda:%d" % (name, t.device.index, device))
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError("%s: %d bytes, the plan needs %d" % (name, t.numel() * t.element_size(), nbytes))
     return ctypes.c_void_p(t.data_ptr())
 
 
@@ -125,6 +139,18 @@ class Plan:
         h = ctypes.c_void_p()
         _check("dqgan_plan_create", load().dqgan_plan_create(ctypes.byref(self.desc), ctypes.byref(h)))
         self.handle = h
+        self.device = torch.cuda.current_device()
+        self._wire_bytes = self.wire_bytes()
+
+    # byte sizes of the arguments (include/dqgan.h)
+    def _mat(self, t, name):
+        return _ptr(t, name, 4 * self.M * self.ld, F32, self.device)
+
+    def _vec(self, t, name):
+        return _ptr(t, name, 4 * self.ld, F32, self.device)
+
+    def _scales(self, t, name):
+        return _ptr(t, name, 4 * self.M * self.n_seg, F32, self.device)
 
     @classmethod
     def from_workload(cls, w):
@@ -161,53 +187,66 @@ class Wire:
     def __init__(self, sign=None, level=None, scale=None, val=None, idx=None):
         self.sign, self.level, self.scale, self.val, self.idx = sign, level, scale, val, idx
 
-    def struct(self):
-        return WireStruct(*[None if t is None else _ptr(t).value for t in
-                            (self.sign, self.level, self.scale, self.val, self.idx)])
+    def struct(self, plan):
+        """The dqgan_wire of these planes; each plane the plan's compressor
+        uses must be present and large enough."""
+        planes = (("sign", self.sign, U32), ("level", self.level, U32), ("scale", self.scale, F32),
+                  ("val", self.val, F32), ("idx", self.idx, U32))
+        ptrs = []
+        for (name, t, dt), need in zip(planes, plan._wire_bytes):
+            if need and t is None:
+                raise ValueError("wire.%s: the plan's compressor needs this plane (%d bytes)" % (name, need))
+            p = _ptr(t, "wire." + name, need, dt, plan.device)
+            ptrs.append(None if p is None else p.value)
+        return WireStruct(*ptrs)
 
 
 def compress_ef(plan, eta, t, G, E, scales_in, wire, stream=None):
-    ws = wire.struct()
-    _check("dqgan_compress_ef", load().dqgan_compress_ef(plan.handle, ctypes.c_float(eta), t, _ptr(G), _ptr(E),
-                                                         _ptr(scales_in), ctypes.byref(ws), _stream(stream)))
-
-
-def pack(plan, codes, scales, wire, stream=None):
-    ws = wire.struct()
-    _check("dqgan_pack", load().dqgan_pack(plan.handle, _ptr(codes), _ptr(scales), ctypes.byref(ws),
-                                           _stream(stream)))
-
-
-def unpack(plan, wire, Phat, stream=None):
-    ws = wire.struct()
-    _check("dqgan_unpack", load().dqgan_unpack(plan.handle, ctypes.byref(ws), _ptr(Phat), _stream(stream)))
-
-
-def aggregate(plan, wire, Qhat, stream=None):
-    ws = wire.struct()
-    _check("dqgan_aggregate", load().dqgan_aggregate(plan.handle, ctypes.byref(ws), _ptr(Qhat), _stream(stream)))
-
-
-def omd_step(plan, eta, Qhat, W, G, E, WX, stream=None):
-    _check("dqgan_omd_step", load().dqgan_omd_step(plan.handle, ctypes.c_float(eta), _ptr(Qhat), _ptr(W), _ptr(G),
-                                                   _ptr(E), _ptr(WX), _stream(stream)))
-
-
-def step_fused(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
-    ws = wire.struct()
-    _check("dqgan_step_fused", load().dqgan_step_fused(plan.handle, ctypes.c_float(eta), t, _ptr(G), _ptr(E),
-                                                       _ptr(W), _ptr(WX), ctypes.byref(ws), _ptr(Qhat),
-                                                       _stream(stream)))
-
-
-def step_scales(plan, eta, G, E, wire, stream=None):
-    ws = wire.struct()
-    _check("dqgan_step_scales", load().dqgan_step_scales(plan.handle, ctypes.c_float(eta), _ptr(G), _ptr(E),
+    ws = wire.struct(plan)
+    _check("dqgan_compress_ef", load().dqgan_compress_ef(plan.handle, ctypes.c_float(eta), t, plan._mat(G, "G"),
+                                                         plan._mat(E, "E"), plan._scales(scales_in, "scales_in"),
                                                          ctypes.byref(ws), _stream(stream)))
 
 
+def pack(plan, codes, scales, wire, stream=None):
+    ws = wire.struct(plan)
+    _check("dqgan_pack", load().dqgan_pack(plan.handle, _ptr(codes, "codes", 2 * plan.M * plan.ld, U16, plan.device),
+                                           plan._scales(scales, "scales"), ctypes.byref(ws), _stream(stream)))
+
+
+def unpack(plan, wire, Phat, stream=None):
+    ws = wire.struct(plan)
+    _check("dqgan_unpack", load().dqgan_unpack(plan.handle, ctypes.byref(ws), plan._mat(Phat, "Phat"),
+                                               _stream(stream)))
+
+
+def aggregate(plan, wire, Qhat, stream=None):
+    ws = wire.struct(plan)
+    _check("dqgan_aggregate", load().dqgan_aggregate(plan.handle, ctypes.byref(ws), plan._vec(Qhat, "Qhat"),
+                                                     _stream(stream)))
+
+
+def omd_step(plan, eta, Qhat, W, G, E, WX, stream=None):
+    _check("dqgan_omd_step", load().dqgan_omd_step(plan.handle, ctypes.c_float(eta), plan._vec(Qhat, "Qhat"),
+                                                   plan._vec(W, "W"), plan._mat(G, "G"), plan._mat(E, "E"),
+                                                   plan._mat(WX, "WX"), _stream(stream)))
+
+
+def step_fused(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
+    ws = wire.struct(plan)
+    _check("dqgan_step_fused", load().dqgan_step_fused(plan.handle, ctypes.c_float(eta), t, plan._mat(G, "G"),
+                                                       plan._mat(E, "E"), plan._vec(W, "W"), plan._mat(WX, "WX"),
+                                                       ctypes.byref(ws), plan._vec(Qhat, "Qhat"), _stream(stream)))
+
+
+def step_scales(plan, eta, G, E, wire, stream=None):
+    ws = wire.struct(plan)
+    _check("dqgan_step_scales", load().dqgan_step_scales(plan.handle, ctypes.c_float(eta), plan._mat(G, "G"),
+                                                         plan._mat(E, "E"), ctypes.byref(ws), _stream(stream)))
+
+
 def step_apply(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
-    ws = wire.struct()
-    _check("dqgan_step_apply", load().dqgan_step_apply(plan.handle, ctypes.c_float(eta), t, _ptr(G), _ptr(E),
-                                                       _ptr(W), _ptr(WX), ctypes.byref(ws), _ptr(Qhat),
-                                                       _stream(stream)))
+    ws = wire.struct(plan)
+    _check("dqgan_step_apply", load().dqgan_step_apply(plan.handle, ctypes.c_float(eta), t, plan._mat(G, "G"),
+                                                       plan._mat(E, "E"), plan._vec(W, "W"), plan._mat(WX, "WX"),
+                                                       ctypes.byref(ws), plan._vec(Qhat, "Qhat"), _stream(stream)))
