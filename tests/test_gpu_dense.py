@@ -235,3 +235,36 @@ def test_free_running_configs(index, steps):
         exact += int(np.array_equal(gpu["E"][:, :d], ref["E"][:, :d]))
     s.close()
     print("steps with identical residuals: %d of %d" % (exact, steps))
+
+
+PAD_CASES = {
+    "sign_m20": lambda: custom(d=4001, M=20, kind="sign", seg_offsets=[0, 77, 4001], eta=1e-2, seed=51,
+                               ld=4096 + 2048),
+    "qsgd15_m3": lambda: custom(d=3000, M=3, kind="qsgd", levels=15, seg_offsets=[0, 1500, 3000], eta=1e-2,
+                                seed=52, ld=3072 + 4096),
+    "mbit8_m9": lambda: custom(d=2050, M=9, kind="mbit", levels=8, norm="linf", eta=1e-2, seed=53, ld=3072 + 1024),
+    "topk_m3": lambda: custom(d=5000, M=3, kind="topk", k=100, eta=1e-2, seed=54, ld=5120 + 3072),
+    "identity_m2": lambda: custom(d=999, M=2, kind="identity", eta=1e-2, seed=55, ld=1024 + 1024),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PAD_CASES))
+def test_padding_is_never_read(name):
+    """Row strides with whole padding tiles beyond d, NaN in the padding of
+    the gradients and sentinels in that of e and w: results on [0, d) equal
+    the oracle's, the padding of E and W is untouched, that of WX and q-hat
+    is written as 0."""
+    w = PAD_CASES[name]()
+    assert w.ld >= (w.d + 1023) // 1024 * 1024 + 1024
+    G, E, W = inputs(w)
+    G[:, w.d:] = np.nan
+    E[:, w.d:] = 7.0
+    W[w.d:] = -3.0
+    print("case", name, "d", w.d, "ld", w.ld, "M", w.M, flush=True)
+    s = GpuState(w, G, E, W)
+    s.fused(1)
+    gpu = s.host()
+    s.close()
+    ref = _oracle(w, G, E, W, scales_in=gpu.get("scale"))
+    compare_step(w, gpu, ref)
+    assert np.all(gpu["E"][:, w.d:] == 7.0) and np.all(gpu["W"][w.d:] == -3.0)
