@@ -270,7 +270,7 @@ def main():
         print("bench: timing the oracle on a sample", file=sys.stderr, flush=True)
         # about 10-30 s of single-core work: the sort-based top-k oracle is
         # slower per element than the quantizers'
-        out["cpu_baseline"] = cpu_baseline(w, 4_000_000 if w.kind == "topk" else 12_000_000)
+        out["cpu_baseline"] = cpu_baseline(w, 4_000_000 if w.kind == "topk" else 18_000_000)
     print(json.dumps(out), flush=True)
 
 
