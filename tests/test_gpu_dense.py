@@ -268,3 +268,24 @@ def test_padding_is_never_read(name):
     ref = _oracle(w, G, E, W, scales_in=gpu.get("scale"))
     compare_step(w, gpu, ref)
     assert np.all(gpu["E"][:, w.d:] == 7.0) and np.all(gpu["W"][w.d:] == -3.0)
+
+
+@pytest.mark.parametrize("kind,extra", [("sign", {}), ("qsgd", {"levels": 15}), ("qsgd", {"levels": 255, "norm": "linf"}),
+                                        ("mbit", {"levels": 8, "norm": "linf"}), ("mbit", {"levels": 4, "norm": "l2"})])
+def test_denormal_segment(kind, extra):
+    """A segment whose p is denormal (|p| ~ 1e-41, so s / sigma overflows
+    binary32 for the quantizers) next to a normal one: bit-exact against the
+    oracle, denormals kept."""
+    w = custom(d=3000, M=4, kind=kind, seg_offsets=[0, 1000, 3000], eta=1.0, seed=61, group_scale=[1e-41, 1e-3],
+               **extra)
+    G, E, W = inputs(w, e_scale=0.0)
+    assert np.abs(G[:, :1000]).max() < 1.2e-38 and np.count_nonzero(G[:, :1000]) > 3000
+    print("case", kind, extra, flush=True)
+    s = GpuState(w, G, E, W)
+    s.fused(1)
+    gpu = s.host()
+    s.close()
+    own = _oracle(w, G, E, W)
+    np.testing.assert_allclose(gpu["scale"], own["scale"], rtol=1e-5, atol=0)
+    ref = _oracle(w, G, E, W, scales_in=gpu["scale"])
+    compare_step(w, gpu, ref)
