@@ -2,7 +2,8 @@
 bench.py times (dqgan_step_scales then dqgan_step_apply), on the gradient
 batches bench.py draws.
 
-C2 (d = 6.3M, M = 16, s = 255): every output against the oracle.
+C2 (d = 6.3M, M = 16, s = 255) and C5 (the same shape, 8-bit Appendix A
+codes, infinity norm): every output against the oracle.
 C3 (d = 33.5M, M = 32, s = 15): sampled segments (the smallest, a middle one,
 the largest), all workers, element by element against the oracle.
 C4 (d = 1e8, M = 64, top-k k = 1e6): sampled workers checked for the exact
@@ -52,18 +53,22 @@ def _release_memory():
 
 
 @pytest.mark.timeout(300)
-def test_c2_full_teacher_forced():
+@pytest.mark.parametrize("index", [2, 5])
+def test_c2_c5_full_teacher_forced(index):
+    """C2: 8-bit s-level quantizer, L2; C5: the same shape with the paper's
+    8-bit sign-magnitude codes and the infinity-norm scale.  Every output."""
     from oracle import oracle as orc
     import synth
     from gpu_common import compare_step
-    w = synth.get(2)
-    print("C2 full", flush=True)
+    w = synth.get(index)
+    print("C%d full" % index, flush=True)
     plan, G, pre, E, W, WX, wire = _run(w)
     t = 2
     gpu = {"E": E.cpu().numpy(), "W": W.cpu().numpy(), "WX": WX.cpu().numpy(),
            "scale": wire.scale.view(w.M, w.n_seg).cpu().numpy(),
-           "sign": wire.sign.view(w.M, -1).cpu().numpy().view(np.uint32),
            "level": wire.level.view(w.M, -1).cpu().numpy().view(np.uint32)}
+    if wire.sign is not None:
+        gpu["sign"] = wire.sign.view(w.M, -1).cpu().numpy().view(np.uint32)
     Gh, Eh, Wh = G.cpu().numpy(), pre["E"].cpu().numpy(), pre["W"].cpu().numpy()
     plan.close()
     ref = orc.step(w.as_dict(), np.float32(w.eta), t, Gh, Eh.copy(), Wh.copy(), scales_in=gpu["scale"])
