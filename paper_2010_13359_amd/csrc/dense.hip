@@ -285,7 +285,7 @@ __device__ __forceinline__ void lookup_segments(const int64_t *__restrict__ off,
     }
 }
 
-// Message stores for one quad of one row.
+// Message stores for one quad of one row (every lane of the wave active).
 template <int KIND, int LB>
 __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, uint32_t *__restrict__ level_row,
                                               float *__restrict__ val_row, int64_t q, const QuadCodes &cq) {
@@ -298,9 +298,7 @@ __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, u
             level_row[q] = cq.levels;
         } else {
             const uint32_t l = cq.levels;
-            const uint16_t h = static_cast<uint16_t>((l & 0xFu) | ((l >> 4) & 0xF0u) | ((l >> 8) & 0xF00u) |
-                                                     ((l >> 12) & 0xF000u));
-            reinterpret_cast<uint16_t *>(level_row)[q] = h;
+            store_fields16(level_row, q, (l & 0xFu) | ((l >> 4) & 0xF0u) | ((l >> 8) & 0xF00u) | ((l >> 12) & 0xF000u));
         }
     }
     if (KIND == kMbit) {
@@ -309,9 +307,9 @@ __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, u
         if (LB == 8) {
             level_row[q] = l | ((nib & 1u) << 7) | ((nib & 2u) << 14) | ((nib & 4u) << 21) | ((nib & 8u) << 28);
         } else {
-            const uint32_t h = (l & 0x7u) | ((l >> 4) & 0x70u) | ((l >> 8) & 0x700u) | ((l >> 12) & 0x7000u) |
-                               ((nib & 1u) << 3) | ((nib & 2u) << 6) | ((nib & 4u) << 9) | ((nib & 8u) << 12);
-            reinterpret_cast<uint16_t *>(level_row)[q] = static_cast<uint16_t>(h);
+            store_fields16(level_row, q,
+                           (l & 0x7u) | ((l >> 4) & 0x70u) | ((l >> 8) & 0x700u) | ((l >> 12) & 0x7000u) |
+                               ((nib & 1u) << 3) | ((nib & 2u) << 6) | ((nib & 4u) << 9) | ((nib & 8u) << 12));
         }
     }
     if (KIND == kIdentity) st4(val_row + 4 * q, cq.phat);

@@ -65,6 +65,24 @@ __device__ __forceinline__ uint32_t or_reduce8_to_lane4(uint32_t x) {
     return x;
 }
 
+// Store of a 4-bit field plane: each lane holds the 16 bits of its quad; lane
+// pairs form a word (quad_perm 1,0,3,2), lane 8j gathers the words of lanes
+// 8j+2, 8j+4, 8j+6 (row shifts left by 2, 4, 6) and writes the group's 16
+// bytes with one streaming 128-bit store.  Sub-dword stores of the same bytes
+// made the fused pass several percent slower than its compute-free access
+// pattern.  Every lane of the wave must be active; `row` is 16-byte aligned
+// and lane 8j holds quad q with q % 8 == 0.
+__device__ __forceinline__ void store_fields16(uint32_t *__restrict__ row, int64_t q, uint32_t h) {
+    const uint32_t hp = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(h), 0xB1, 0xF, 0xF, true));
+    const uint32_t wv = (h & 0xFFFFu) | (hp << 16);
+    u32x4 v;
+    v.x = wv;
+    v.y = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(wv), 0x102, 0xF, 0xF, true));
+    v.z = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(wv), 0x104, 0xF, 0xF, true));
+    v.w = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(wv), 0x106, 0xF, 0xF, true));
+    if ((q & 7) == 0) __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(row + (q >> 1)));
+}
+
 // Segment of element i, scanning forward from segment j (offsets ascending).
 __device__ __forceinline__ int seg_from(const int64_t *__restrict__ off, int j, int64_t i) {
     while (off[j + 1] <= i) ++j;
