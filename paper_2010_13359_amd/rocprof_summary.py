@@ -2,7 +2,7 @@
 dispatch count and duration statistics, and for counter runs the mean value of
 each counter per dispatch.
 
-    python -m paper_2010_13359_amd.rocprof_summary RESULTS.db [--counters]
+    python -m paper_2010_13359_amd.rocprof_summary RESULTS.db [--skip-first N | --counters | --dispatches NAME]
 """
 import argparse
 import re
@@ -28,9 +28,11 @@ def short_name(name):
     return s if len(s) <= 90 else s[:87] + "..."
 
 
-def kernel_stats(db):
+def kernel_stats(db, skip_first=0):
+    """Per kernel: dispatch count and duration statistics, leaving out the
+    first `skip_first` dispatches of each kernel (warmup iterations)."""
     con = sqlite3.connect(db)
-    rows = con.execute("select name, duration from kernels").fetchall()
+    rows = con.execute("select name, duration from kernels order by start").fetchall()
     agg = {}
     for name, dur in rows:
         key = short_name(name)
@@ -38,6 +40,7 @@ def kernel_stats(db):
         a.append(float(dur))
     out = []
     for k, v in agg.items():
+        v = v[skip_first:] if len(v) > skip_first else v
         v.sort()
         out.append((k, len(v), sum(v) / len(v) / 1e3, v[len(v) // 2] / 1e3, v[0] / 1e3, v[-1] / 1e3, sum(v) / 1e3))
     out.sort(key=lambda r: -r[6])
@@ -60,11 +63,36 @@ def counter_stats(db):
     return out
 
 
+def counter_dispatches(db, match):
+    """Per dispatch of kernels whose name contains `match`: grid size and
+    counter values (for the copy-kernel calibration of the byte counters)."""
+    con = sqlite3.connect(db)
+    cols = [r[1] for r in con.execute("pragma table_info(counters_collection)")]
+    grid = next((c for c in ("grid_size_x", "grid_x", "grid_size") if c in cols), None)
+    rows = con.execute("select kernel_name, counter_name, dispatch_id, value, %s from counters_collection"
+                       % (grid or "0")).fetchall()
+    per = {}
+    for name, ctr, disp, val, grid in rows:
+        if match not in name:
+            continue
+        d = per.setdefault(disp, {"kernel": short_name(name), "grid": grid})
+        d[ctr] = d.get(ctr, 0.0) + float(val)
+    return [dict(v, dispatch=k) for k, v in sorted(per.items())]
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("db")
     ap.add_argument("--counters", action="store_true")
+    ap.add_argument("--dispatches", metavar="NAME", help="per-dispatch counters of kernels whose name contains NAME")
+    ap.add_argument("--skip-first", type=int, default=0, metavar="N",
+                    help="leave out the first N dispatches of each kernel (warmup) from the duration statistics")
     a = ap.parse_args(argv)
+    if a.dispatches:
+        for d in counter_dispatches(a.db, a.dispatches):
+            vals = "  ".join("%s=%.1f" % (k, v) for k, v in d.items() if k not in ("kernel", "grid", "dispatch"))
+            print("dispatch %-6d %-40s grid %-10s %s" % (d["dispatch"], d["kernel"][:40], d["grid"], vals))
+        return 0
     if a.counters:
         print("%-60s %-12s %8s %16s" % ("kernel", "counter", "calls", "mean/dispatch"))
         for k, ctr, n, mean in counter_stats(a.db):
@@ -72,7 +100,7 @@ def main(argv=None):
     else:
         print("%-60s %6s %12s %12s %12s %12s %14s" % ("kernel", "calls", "avg_us", "median_us", "min_us", "max_us",
                                                        "total_us"))
-        for k, n, avg, med, mn, mx, tot in kernel_stats(a.db):
+        for k, n, avg, med, mn, mx, tot in kernel_stats(a.db, a.skip_first):
             print("%-60s %6d %12.1f %12.1f %12.1f %12.1f %14.1f" % (k[:60], n, avg, med, mn, mx, tot))
     return 0
 
