@@ -285,8 +285,9 @@ __device__ __forceinline__ void lookup_segments(const int64_t *__restrict__ off,
     }
 }
 
-// Message stores for one quad of one row (every lane of the wave active).
-template <int KIND, int LB>
+// Message stores for one quad of one row (every lane of the wave active);
+// STREAM: an 8-bit plane larger than the Infinity Cache (store_fields32).
+template <int KIND, int LB, bool STREAM>
 __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, uint32_t *__restrict__ level_row,
                                               float *__restrict__ val_row, int64_t q, const QuadCodes &cq) {
     if (KIND == kSign || KIND == kQsgd) {
@@ -295,7 +296,7 @@ __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, u
     }
     if (KIND == kQsgd) {
         if (LB == 8) {
-            level_row[q] = cq.levels;
+            store_fields32<STREAM>(level_row, q, cq.levels);
         } else {
             const uint32_t l = cq.levels;
             store_fields16(level_row, q, (l & 0xFu) | ((l >> 4) & 0xF0u) | ((l >> 8) & 0xF00u) | ((l >> 12) & 0xF000u));
@@ -305,7 +306,8 @@ __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, u
         // m-bit sign-magnitude codes: the sign bit on top of each field
         const uint32_t nib = cq.sign_nib, l = cq.levels;
         if (LB == 8) {
-            level_row[q] = l | ((nib & 1u) << 7) | ((nib & 2u) << 14) | ((nib & 4u) << 21) | ((nib & 8u) << 28);
+            const uint32_t code = l | ((nib & 1u) << 7) | ((nib & 2u) << 14) | ((nib & 4u) << 21) | ((nib & 8u) << 28);
+            store_fields32<STREAM>(level_row, q, code);
         } else {
             store_fields16(level_row, q,
                            (l & 0x7u) | ((l >> 4) & 0x70u) | ((l >> 8) & 0x700u) | ((l >> 12) & 0x7000u) |
@@ -315,6 +317,18 @@ __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, u
     if (KIND == kIdentity) st4(val_row + 4 * q, cq.phat);
 }
 
+// store_message with the store kind chosen at run time (kernels off the
+// fused step's hot loop).
+template <int KIND, int LB>
+__device__ __forceinline__ void store_message_rt(uint32_t *__restrict__ sign_row, uint32_t *__restrict__ level_row,
+                                                 float *__restrict__ val_row, int64_t q, const QuadCodes &cq,
+                                                 bool stream) {
+    if (stream)
+        store_message<KIND, LB, true>(sign_row, level_row, val_row, q, cq);
+    else
+        store_message<KIND, LB, false>(sign_row, level_row, val_row, q, cq);
+}
+
 struct RowArgs {
     float eta;
     uint32_t t;
@@ -322,6 +336,7 @@ struct RowArgs {
     int32_t M, n_seg, s;
     uint32_t k0, k1;
     int64_t sign_words, level_words;  // words per row of each plane
+    int32_t stream_msg;               // message planes larger than the Infinity Cache: streaming stores
 };
 
 // Worker side only (dqgan_compress_ef): one (quad, worker) per thread.
@@ -343,7 +358,8 @@ __global__ __launch_bounds__(kBlock) void k_encode_rows(const float *__restrict_
     const QuadCodes cq =
         encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg, a.s, a.k0, a.k1, a.t);
     st_stream(E + rb + i0, cq.enew);
-    store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq);
+    store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq,
+                               a.stream_msg != 0);
 }
 
 // The fused step.  MT > 0: M == MT, the extrapolation operands stay in
@@ -371,7 +387,8 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
         const QuadCodes cq = encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg,
                                                a.s, a.k0, a.k1, a.t);
         st_stream(E + rb + i0, cq.enew);
-        store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq);
+        store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq,
+                                   a.stream_msg != 0);
         if (m == 0) {
             acc = cq.phat;
         } else {
@@ -426,7 +443,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
 // 0..g-1, so the result is the same sequential binary32 sum as in the
 // one-lane-per-quad kernel.  Few registers per lane leave room for many
 // waves per SIMD, which keeps enough loads in flight to stream from HBM.
-template <int KIND, int LB, int R, int NG>
+template <int KIND, int LB, int R, int NG, bool STREAM>
 __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict__ G, float *__restrict__ E,
                                                          float *__restrict__ W, float *__restrict__ WX,
                                                          float *__restrict__ Qhat, uint32_t *__restrict__ sign_plane,
@@ -473,8 +490,8 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
             if constexpr (KIND == kTopk) {
                 store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + blockIdx.x], i0, cq);
             } else {
-                store_message<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q,
-                                        cq);
+                store_message<KIND, LB, STREAM>(sign_plane + m * a.sign_words, level_plane + m * a.level_words,
+                                                val + rb, q, cq);
             }
             ph[r] = cq.phat;
 #pragma unroll
@@ -681,11 +698,12 @@ __global__ __launch_bounds__(kBlock) void k_pack(const uint16_t *__restrict__ co
         cq.levels |= (c4[c] & fmask) << (8 * c);
     }
     if (KIND == kSign)
-        store_message<kSign, 0>(sign_plane + m * a.sign_words, nullptr, nullptr, q, cq);
+        store_message_rt<kSign, 0>(sign_plane + m * a.sign_words, nullptr, nullptr, q, cq, a.stream_msg != 0);
     else if (KIND == kMbit)
-        store_message<kMbit, LB>(nullptr, level_plane + m * a.level_words, nullptr, q, cq);
+        store_message_rt<kMbit, LB>(nullptr, level_plane + m * a.level_words, nullptr, q, cq, a.stream_msg != 0);
     else
-        store_message<kQsgd, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, nullptr, q, cq);
+        store_message_rt<kQsgd, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, nullptr, q,
+                                    cq, a.stream_msg != 0);
 }
 
 // Top-k worker side only (dqgan_compress_ef): one wave per (tile, worker).
@@ -716,6 +734,8 @@ RowArgs row_args(const dqgan_plan_s &P, float eta, uint32_t t) {
     a.k1 = static_cast<uint32_t>(P.desc.seed >> 32);
     a.sign_words = P.desc.ld / 32;
     a.level_words = P.level_bits ? P.desc.ld * P.level_bits / 32 : 0;
+    const double msg_bytes = 4.0 * P.desc.M * static_cast<double>(a.sign_words + a.level_words);
+    a.stream_msg = msg_bytes > kInfinityCacheBytes ? 1 : 0;
     return a;
 }
 
@@ -743,9 +763,15 @@ hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G,
         ta.k = P.desc.k;
         ta.idx = w.idx;
     }
-    hipLaunchKernelGGL((k_fused_split<KIND, LB, R, NG>), dim3(static_cast<unsigned>(P.n_tiles * 4)), dim3(64 * NG), 0,
-                       st, G, E, W, WX, Qhat, w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a,
-                       inv_m(P.desc.M), ta);
+    const dim3 grid(static_cast<unsigned>(P.n_tiles * 4)), block(64 * NG);
+    // Only 8-bit planes have a second store kind (store_fields32).
+    constexpr bool kTwoKinds = (KIND == kQsgd || KIND == kMbit) && LB == 8;
+    if (kTwoKinds && a.stream_msg)
+        hipLaunchKernelGGL((k_fused_split<KIND, LB, R, NG, kTwoKinds>), grid, block, 0, st, G, E, W, WX, Qhat, w.sign,
+                           w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a, inv_m(P.desc.M), ta);
+    else
+        hipLaunchKernelGGL((k_fused_split<KIND, LB, R, NG, false>), grid, block, 0, st, G, E, W, WX, Qhat, w.sign,
+                           w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a, inv_m(P.desc.M), ta);
     return hipGetLastError();
 }
 

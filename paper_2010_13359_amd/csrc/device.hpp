@@ -65,13 +65,16 @@ __device__ __forceinline__ uint32_t or_reduce8_to_lane4(uint32_t x) {
     return x;
 }
 
-// Store of a 4-bit field plane: each lane holds the 16 bits of its quad; lane
-// pairs form a word (quad_perm 1,0,3,2), lane 8j gathers the words of lanes
-// 8j+2, 8j+4, 8j+6 (row shifts left by 2, 4, 6) and writes the group's 16
-// bytes with one streaming 128-bit store.  Sub-dword stores of the same bytes
-// made the fused pass several percent slower than its compute-free access
-// pattern.  Every lane of the wave must be active; `row` is 16-byte aligned
-// and lane 8j holds quad q with q % 8 == 0.
+// Stores of a packed field plane, one quad per lane.  The fields of
+// consecutive lanes are gathered with DPP: lane pairs form a word (quad_perm
+// 1,0,3,2); lane 8j (4-bit fields) or 4j (8-bit fields) collects the next
+// words with row shifts and writes 16 bytes with one non-temporal store.
+// Every lane of the wave must be active; `row` is 16-byte aligned; lane 8j /
+// 4j holds quad q with q % 8 == 0 / q % 4 == 0.
+//
+// 4-bit fields (16 bits per lane): sub-dword stores of the same bytes made
+// the fused pass 9 % slower than its compute-free access pattern; the
+// gathered streaming store runs at the pattern's rate.
 __device__ __forceinline__ void store_fields16(uint32_t *__restrict__ row, int64_t q, uint32_t h) {
     const uint32_t hp = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(h), 0xB1, 0xF, 0xF, true));
     const uint32_t wv = (h & 0xFFFFu) | (hp << 16);
@@ -81,6 +84,25 @@ __device__ __forceinline__ void store_fields16(uint32_t *__restrict__ row, int64
     v.z = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(wv), 0x104, 0xF, 0xF, true));
     v.w = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(wv), 0x106, 0xF, 0xF, true));
     if ((q & 7) == 0) __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(row + (q >> 1)));
+}
+
+// 8-bit fields (32 bits per lane).  STREAM: the plane is larger than the
+// 256 MB Infinity Cache, and the gathered streaming store is 4-5 % faster at
+// C6's 1.07 GB plane; a smaller plane keeps one cache-allocating 32-bit store
+// per lane (streaming made C2's and C5's 0.1 GB planes 5 % slower: the cache
+// defers their write-back past the pass).
+template <bool STREAM>
+__device__ __forceinline__ void store_fields32(uint32_t *__restrict__ row, int64_t q, uint32_t w) {
+    if (!STREAM) {
+        row[q] = w;
+        return;
+    }
+    u32x4 v;
+    v.x = w;
+    v.y = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(w), 0x101, 0xF, 0xF, true));
+    v.z = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(w), 0x102, 0xF, 0xF, true));
+    v.w = static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(w), 0x103, 0xF, 0xF, true));
+    if ((q & 3) == 0) __builtin_nontemporal_store(v, reinterpret_cast<u32x4 *>(row + q));
 }
 
 // Segment of element i, scanning forward from segment j (offsets ascending).

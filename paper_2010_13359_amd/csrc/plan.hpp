@@ -19,6 +19,10 @@ struct Piece {
 };
 constexpr int64_t kPieceElems = 16384;
 
+// Capacity of the MI355X Infinity Cache (memory-side, in front of HBM): the
+// fused pass streams message planes larger than this past the caches.
+constexpr double kInfinityCacheBytes = 256.0 * 1024 * 1024;
+
 // Per-worker selection state of the top-k compressor.  Keys are the binary32
 // bit patterns of |p| (monotone in |p|).  Element i is selected iff
 // key > T, or key == T and i <= I.
