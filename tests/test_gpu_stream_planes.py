@@ -8,8 +8,10 @@ sign-magnitude codes.
 The iteration is checked against the oracle, teacher-forced with the GPU's
 segment scales, on windows at the start of the row, across a segment
 boundary, in the middle and at the ragged end; the scales of the sampled
-segments against the oracle's own within 1e-5.  Inputs are drawn on the
-device; only windows are copied to the host.
+segments against the oracle's own within 1e-5.  Also with M = 130 (the
+one-lane kernel), and for the worker side alone (dqgan_compress_ef) and
+dqgan_pack, which choose the store kind at run time.  Inputs are drawn on
+the device; only windows are copied to the host.
 """
 import numpy as np
 import pytest
@@ -43,51 +45,45 @@ def _words(plane_row, a, b, bits):
     return plane_row[a // per:(b + per - 1) // per].cpu().numpy().view(np.uint32)
 
 
-@pytest.mark.timeout(600)
-@pytest.mark.parametrize("case", CASES, ids=lambda c: "%s%d" % (c[0], c[1]))
-def test_streamed_plane_windows(case):
+def _device_state(w, seed):
+    """Device inputs: g ~ N(0,1), e_{t-1} ~ N(0, 1e-3^2), w ~ N(0, 0.02^2); padding zero."""
     import torch
-    from oracle import oracle as orc
-    from paper_2010_13359_amd import dqgan
-    kind, levels, norm, d = case
-    M = 16
-    offs = [0, 4_000_003, d - 50_000, d]
-    w = custom(d=d, M=M, kind=kind, levels=levels, norm=norm, seg_offsets=offs, eta=1e-3, seed=41)
-    bits = (9 if levels == 255 else 5) if kind == "qsgd" else levels
-    assert M * w.ld * bits / 8 > 256 * 2 ** 20
-    print("streamed plane %s %d: d=%d" % (kind, levels, d), flush=True)
     dev = torch.device("cuda:0")
     gen = torch.Generator(device=dev)
-    gen.manual_seed(41)
-    G = torch.zeros((M, w.ld), dtype=torch.float32, device=dev)
+    gen.manual_seed(seed)
+    G = torch.zeros((w.M, w.ld), dtype=torch.float32, device=dev)
     E = torch.zeros_like(G)
     W = torch.zeros(w.ld, dtype=torch.float32, device=dev)
-    G[:, :d].normal_(0.0, 1.0, generator=gen)
-    E[:, :d].normal_(0.0, 1e-3, generator=gen)
-    W[:d].normal_(0.0, 0.02, generator=gen)
-    E0, W0 = E.clone(), W.clone()
-    plan = dqgan.Plan.from_workload(w)
-    WX = torch.empty_like(G)
-    wire = plan.new_wire(dev)
-    t = 3
-    dqgan.step_fused(plan, w.eta, t, G, E, W, WX, wire)
-    torch.cuda.synchronize()
+    G[:, :w.d].normal_(0.0, 1.0, generator=gen)
+    E[:, :w.d].normal_(0.0, 1e-3, generator=gen)
+    W[:w.d].normal_(0.0, 0.02, generator=gen)
+    return G, E, W
+
+
+def _windows(w):
+    """Windows [a, b) (a a multiple of 32): the start of the row, across the
+    first segment boundary, the middle, the ragged end."""
+    d, o1 = w.d, w.seg_offsets[1] // 32 * 32
+    mid = d // 2 // 32 * 32
+    return [(0, 8192), (max(0, o1 - 4096), o1 + 4096), (mid, mid + 8192), (d // 32 * 32 - 8192, d)]
+
+
+def _check_windows(w, t, G, E0, W0, E, W, WX, wire, rows=None):
+    """Teacher-forced oracle check of one iteration on windows of the row,
+    with the GPU's segment scales, for the worker rows `rows` (all if None;
+    the server average always uses every worker)."""
+    from oracle import oracle as orc
+    M = w.M
     scales = wire.scale.view(M, w.n_seg).cpu().numpy()
-    mbit = kind == "mbit"
-    k_levels = (1 << (levels - 1)) - 1 if mbit else levels
+    mbit = w.kind == "mbit"
+    k_levels = (1 << (w.levels - 1)) - 1 if mbit else w.levels
+    lbits = w.levels if mbit else (8 if w.levels == 255 else 4)
     sign_rows = None if mbit else wire.sign.view(M, -1)
     level_rows = wire.level.view(M, -1)
     eta = np.float32(w.eta)
-    # the sampled segments' scales against the oracle's own
-    for j in (0, 2):
-        a, b = offs[j], offs[j + 1]
-        for m in (0, M - 1):
-            p = orc.ef_accumulate(eta, G[m, a:b].cpu().numpy(), E0[m, a:b].cpu().numpy())
-            own = float(orc.scale(p, w.norm))
-            assert abs(float(scales[m, j]) - own) <= 1e-5 * own, (j, m, float(scales[m, j]), own)
-    windows = [(0, 8192), (offs[1] // 32 * 32 - 4096, offs[1] // 32 * 32 + 4096), (d // 2 // 32 * 32, d // 2 // 32 * 32 + 8192),
-               (d // 32 * 32 - 8192, d)]
-    for a, b in windows:
+    offs = w.seg_offsets
+    check_rows = set(range(M)) if rows is None else set(rows)
+    for a, b in _windows(w):
         n = b - a
         Gs = G[:, a:b].cpu().numpy()
         Es = E0[:, a:b].cpu().numpy()
@@ -96,26 +92,144 @@ def test_streamed_plane_windows(case):
         enew = np.empty((M, n), np.float32)
         for m in range(M):
             p = orc.ef_accumulate(eta, Gs[m], Es[m])
-            # the window may straddle a segment boundary: encode each part with its scale
+            # the window may straddle a segment boundary: each part with its scale
             for j in range(w.n_seg):
                 lo, hi = max(a, offs[j]), min(b, offs[j + 1])
                 if lo >= hi:
                     continue
                 sb, lv, ph, e = orc.qsgd_encode(p[lo - a:hi - a], scales[m, j], k_levels, w.quant_seed, m, t, i0=lo)
                 phat[m, lo - a:hi - a], enew[m, lo - a:hi - a] = ph, e
+                if m not in check_rows:
+                    continue
                 if mbit:
-                    codes = orc.unpack_bits(_words(level_rows[m], a, b, levels), levels, b - a)[lo - a:hi - a]
-                    assert_same("codes [%d,%d) row %d" % (lo, hi, m), codes, orc.mbit_fields(sb, lv, levels))
+                    codes = orc.unpack_bits(_words(level_rows[m], a, b, lbits), lbits, n)[lo - a:hi - a]
+                    assert_same("codes [%d,%d) row %d" % (lo, hi, m), codes, orc.mbit_fields(sb, lv, w.levels))
                 else:
-                    gs = orc.unpack_bits(_words(sign_rows[m], a, b, 1), 1, b - a)[lo - a:hi - a]
-                    gl = orc.unpack_bits(_words(level_rows[m], a, b, 8 if levels == 255 else 4),
-                                         8 if levels == 255 else 4, b - a)[lo - a:hi - a]
+                    gs = orc.unpack_bits(_words(sign_rows[m], a, b, 1), 1, n)[lo - a:hi - a]
+                    gl = orc.unpack_bits(_words(level_rows[m], a, b, lbits), lbits, n)[lo - a:hi - a]
                     assert_same("sign bits [%d,%d) row %d" % (lo, hi, m), gs, sb.astype(np.uint16))
                     assert_same("levels [%d,%d) row %d" % (lo, hi, m), gl, lv)
-        assert_same("e_t [%d,%d)" % (a, b), E[:, a:b].cpu().numpy(), enew)
+        rs = sorted(check_rows)
+        assert_same("e_t [%d,%d)" % (a, b), E[rs, a:b].cpu().numpy(), enew[rs])
         q = orc.aggregate(phat, n)
         wt = orc.omd_update(q, Ws)
         assert_same("w_t [%d,%d)" % (a, b), W[a:b].cpu().numpy(), wt)
-        wx = np.stack([orc.extrapolate(eta, wt, Gs[m], enew[m]) for m in range(M)])
-        assert_same("WX [%d,%d)" % (a, b), WX[:, a:b].cpu().numpy(), wx)
+        wx = np.stack([orc.extrapolate(eta, wt, Gs[m], enew[m]) for m in rs])
+        assert_same("WX [%d,%d)" % (a, b), WX[rs, a:b].cpu().numpy(), wx)
+
+
+def _plane_bytes(w):
+    bits = (9 if w.levels == 255 else 5) if w.kind == "qsgd" else w.levels
+    return w.M * w.ld * bits / 8
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "%s%d" % (c[0], c[1]))
+def test_streamed_plane_windows(case):
+    """The fused pass (two rows per wave) with each field width streamed."""
+    import torch
+    from oracle import oracle as orc
+    from paper_2010_13359_amd import dqgan
+    kind, levels, norm, d = case
+    offs = [0, 4_000_003, d - 50_000, d]
+    w = custom(d=d, M=16, kind=kind, levels=levels, norm=norm, seg_offsets=offs, eta=1e-3, seed=41)
+    assert _plane_bytes(w) > 256 * 2 ** 20
+    print("streamed plane %s %d: d=%d" % (kind, levels, d), flush=True)
+    G, E, W = _device_state(w, 41)
+    E0, W0 = E.clone(), W.clone()
+    plan = dqgan.Plan.from_workload(w)
+    WX = torch.empty_like(G)
+    wire = plan.new_wire(G.device)
+    t = 3
+    dqgan.step_fused(plan, w.eta, t, G, E, W, WX, wire)
+    torch.cuda.synchronize()
+    # the sampled segments' scales against the oracle's own
+    scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
+    eta = np.float32(w.eta)
+    for j in (0, 2):
+        a, b = offs[j], offs[j + 1]
+        for m in (0, w.M - 1):
+            p = orc.ef_accumulate(eta, G[m, a:b].cpu().numpy(), E0[m, a:b].cpu().numpy())
+            own = float(orc.scale(p, w.norm))
+            assert abs(float(scales[m, j]) - own) <= 1e-5 * own, (j, m, float(scales[m, j]), own)
+    _check_windows(w, t, G, E0, W0, E, W, WX, wire)
+    plan.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("kind,levels,d", [("qsgd", 255, 2_300_001), ("mbit", 4, 4_500_003)])
+def test_streamed_plane_many_workers(kind, levels, d):
+    """M = 130: the one-lane-per-quad fused kernel, which picks the store kind
+    at run time."""
+    import torch
+    from paper_2010_13359_amd import dqgan
+    w = custom(d=d, M=130, kind=kind, levels=levels, norm="l2", seg_offsets=[0, 1_000_001, d], eta=1e-3, seed=43)
+    assert _plane_bytes(w) > 256 * 2 ** 20
+    print("streamed plane, M = 130: %s %d d=%d" % (kind, levels, d), flush=True)
+    G, E, W = _device_state(w, 43)
+    E0, W0 = E.clone(), W.clone()
+    plan = dqgan.Plan.from_workload(w)
+    WX = torch.empty_like(G)
+    wire = plan.new_wire(G.device)
+    t = 2
+    dqgan.step_fused(plan, w.eta, t, G, E, W, WX, wire)
+    torch.cuda.synchronize()
+    _check_windows(w, t, G, E0, W0, E, W, WX, wire, rows=(0, 1, 64, 65, 128, 129))
+    plan.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("kind,levels", [("qsgd", 255), ("mbit", 4)])
+def test_streamed_plane_worker_side_and_pack(kind, levels):
+    """dqgan_compress_ef and dqgan_pack (run-time store kind) on streamed
+    planes: the worker side writes the fused iteration's message bit for bit,
+    and pack of random codes matches the oracle's packing on windows."""
+    import torch
+    from oracle import oracle as orc
+    from paper_2010_13359_amd import dqgan
+    d = 20_000_003 if kind == "qsgd" else 40_000_007
+    w = custom(d=d, M=16, kind=kind, levels=levels, norm="l2", seg_offsets=[0, 7_000_001, d], eta=1e-3, seed=47)
+    assert _plane_bytes(w) > 256 * 2 ** 20
+    print("streamed plane, worker side and pack: %s %d" % (kind, levels), flush=True)
+    G, E, W = _device_state(w, 47)
+    E1 = E.clone()
+    plan = dqgan.Plan.from_workload(w)
+    WX = torch.empty_like(G)
+    fused, worker = plan.new_wire(G.device), plan.new_wire(G.device)
+    dqgan.step_fused(plan, w.eta, 4, G, E, W, WX, fused)
+    dqgan.compress_ef(plan, w.eta, 4, G, E1, None, worker)
+    torch.cuda.synchronize()
+    for name in ("sign", "level", "scale"):
+        a, b = getattr(fused, name), getattr(worker, name)
+        if a is not None:
+            assert torch.equal(a, b), name
+    assert torch.equal(E, E1)
+    del E1, WX
+    # pack: random codes with the compressor's level range
+    smax = ((1 << (levels - 1)) - 1) if kind == "mbit" else levels
+    gen = torch.Generator(device=G.device)
+    gen.manual_seed(5)
+    lv = torch.randint(0, smax + 1, (w.M, w.ld), generator=gen, device=G.device, dtype=torch.int32)
+    sg = torch.randint(0, 2, (w.M, w.ld), generator=gen, device=G.device, dtype=torch.int32)
+    codes = ((sg << 15) | lv).to(torch.int16)
+    del lv, sg
+    packed = plan.new_wire(G.device)
+    dqgan.pack(plan, codes, fused.scale, packed)
+    torch.cuda.synchronize()
+    lbits = levels if kind == "mbit" else 8
+    for a, b in _windows(w):
+        c = codes[:, a:b].cpu().numpy().view(np.uint16)
+        for m in (0, w.M - 1):
+            sgn, lvl = (c[m] >> 15).astype(np.uint8), c[m] & 0x7FFF
+            if kind == "mbit":
+                exp = orc.pack_bits(orc.mbit_fields(sgn, lvl, levels), lbits, (b - a + 31) // 32 * lbits)
+                assert_same("packed codes [%d,%d) row %d" % (a, b, m), _words(packed.level.view(w.M, -1)[m], a, b, lbits),
+                            exp[:len(_words(packed.level.view(w.M, -1)[m], a, b, lbits))])
+            else:
+                exp_s = orc.pack_bits(sgn, 1, (b - a + 31) // 32)
+                exp_l = orc.pack_bits(lvl, lbits, (b - a + 31) // 32 * lbits)
+                got_s = _words(packed.sign.view(w.M, -1)[m], a, b, 1)
+                got_l = _words(packed.level.view(w.M, -1)[m], a, b, lbits)
+                assert_same("packed signs [%d,%d) row %d" % (a, b, m), got_s, exp_s[:len(got_s)])
+                assert_same("packed levels [%d,%d) row %d" % (a, b, m), got_l, exp_l[:len(got_l)])
     plan.close()
