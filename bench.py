@@ -262,6 +262,24 @@ def main():
     out["reference_stream"] = {"op": "torch.add(g, e, out=WX) over the step's own [M][ld] buffers (2 reads, 1 write)",
                                "GB/s": round(3 * 4.0 * w.M * w.ld / (ref_t * 1e-3) / 1e9, 1),
                                "ms": round(ref_t, 4)}
+    # Plain copy over the same buffers (1 read, 1 write; torch's vectorized
+    # elementwise kernel, faster here than the runtime's copy kernel): the
+    # reachable rate of a compute-free stream in this process, against which
+    # the dominant kernel's rate is also given.
+    cp_ms = []
+    for _ in range(4):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        torch.mul(Gs[0], 1.0, out=WX)
+        b.record()
+        torch.cuda.synchronize()
+        cp_ms.append(a.elapsed_time(b))
+    cp_t = sorted(cp_ms)[1]
+    cp_gbs = 2 * 4.0 * w.M * w.ld / (cp_t * 1e-3) / 1e9
+    out["copy_ceiling"] = {"op": "torch.mul(g, 1.0, out=WX) over the step's own [M][ld] buffers (1 read, 1 write)",
+                           "GB/s": round(cp_gbs, 1), "ms": round(cp_t, 4),
+                           "roofline_frac_of_copy": round(achieved / cp_gbs, 4),
+                           "step_frac_of_copy": round(step_ach / cp_gbs, 4)}
     del graph
     plan.close()
     del Gs, E, W, WX, wire
