@@ -21,6 +21,7 @@ import hashlib
 import glob
 import json
 import os
+import re
 import sys
 import time
 
@@ -37,15 +38,23 @@ KERNEL_SOURCES = {
 }
 
 
+def _code_only(text):
+    """Source text without comments and blank lines: comment edits do not
+    change what the counters measured."""
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = (re.sub(r"//.*$", "", line).rstrip() for line in text.splitlines())
+    return "\n".join(line for line in lines if line.strip())
+
+
 def source_hash(group="dense"):
-    """Hash of the sources a kernel family is built from (the counters in
-    profiles/traffic.json are valid only for the sources they were taken on)."""
+    """Hash of the code a kernel family is built from (the counters in
+    profiles/traffic.json are valid only for the code they were taken on)."""
     h = hashlib.sha256()
     for name in KERNEL_SOURCES[group]:
         p = os.path.join(ROOT, "paper_2010_13359_amd", "csrc", name)
-        with open(p, "rb") as f:
+        with open(p, encoding="utf-8") as f:
             h.update(os.path.basename(p).encode())
-            h.update(f.read())
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

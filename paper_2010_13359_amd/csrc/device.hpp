@@ -87,10 +87,11 @@ __device__ __forceinline__ void store_fields16(uint32_t *__restrict__ row, int64
 }
 
 // 8-bit fields (32 bits per lane).  STREAM: the plane is larger than the
-// 256 MB Infinity Cache, and the gathered streaming store is 4-5 % faster at
-// C6's 1.07 GB plane; a smaller plane keeps one cache-allocating 32-bit store
-// per lane (streaming made C2's and C5's 0.1 GB planes 5 % slower: the cache
-// defers their write-back past the pass).
+// 256 MB Infinity Cache, where the gathered streaming store is 4-5 % faster
+// (32 workers x 33.5M elements, a 1.07 GB plane); a smaller plane keeps one
+// cache-allocating 32-bit store per lane (streaming made the 0.1 GB planes of
+// 16 workers x 6.3M elements 5 % slower: the cache defers their write-back
+// past the pass).
 template <bool STREAM>
 __device__ __forceinline__ void store_fields32(uint32_t *__restrict__ row, int64_t q, uint32_t w) {
     if (!STREAM) {

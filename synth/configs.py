@@ -1,6 +1,9 @@
-"""The five synthetic workloads (C0..C4): flat fp32 parameter vectors shaped
-like the generator/discriminator pairs of GAN training, split into segments
-(one per layer or per group of layers), with the compressor each uses.
+"""The synthetic workloads C0..C6: flat fp32 parameter vectors shaped like
+the generator/discriminator pairs of GAN training, split into segments (one
+per layer or per group of layers), with the compressor each uses.  C0..C4
+follow the five benchmark shapes; C5 and C6 repeat the shapes of C2 and C3
+with the paper's own experimental compressor (8-bit sign-magnitude codes of
+Appendix A with the infinity-norm scale).
 
 Segment sizes of the two largest workloads are drawn log-uniformly (ratio up
 to 1000 between segments), rounded down to a multiple of 64 elements (at least
