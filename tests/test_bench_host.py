@@ -25,3 +25,17 @@ def test_c3_algorithmic_bytes():
 def test_more_than_one_gpu_is_refused():
     r = subprocess.run([sys.executable, "bench.py", "--gpus", "2"], cwd=bench.ROOT, capture_output=True, text=True)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_code_hash_ignores_comments_only():
+    src = "int a; // count\n/* block\n comment */\nint b;  \n\n"
+    assert bench._code_only(src) == "int a;\nint b;"
+    assert bench._code_only(src) == bench._code_only(src.replace("// count", "// another comment"))
+    assert bench._code_only(src) != bench._code_only(src.replace("int b;", "int c;"))
+
+
+def test_committed_counter_records_match_the_kernel_code():
+    """profiles/traffic.json was taken on the kernel code in the tree (the
+    bench reports its bytes only then)."""
+    for key, group in (("apply_C3", "dense"), ("stats_C3", "dense"), ("apply_C4", "dense"), ("stats_C4", "topk")):
+        assert bench.traffic_record(key, group), key
