@@ -83,7 +83,8 @@ typedef enum {
 
 typedef struct {
     int64_t d;                    /* parameters per worker, d >= 1                 */
-    int64_t ld;                   /* row stride: ld >= d, ld % 1024 == 0           */
+    int64_t ld;                   /* row stride: ld >= d, ld % 1024 == 0,
+                                     ld / 256 <= 2^31 - 1                          */
     int32_t M;                    /* workers, 1 <= M <= 1024                        */
     int32_t n_seg;                /* segments (SIGN, QSGD); 1 for the others        */
     const int64_t *seg_offsets;   /* host, n_seg + 1 entries, strictly increasing,

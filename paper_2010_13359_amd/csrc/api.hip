@@ -39,7 +39,7 @@ dqgan_status optional(const void *p) { return (!p || aligned16(p)) ? DQGAN_OK : 
 dqgan_status validate_desc(const dqgan_desc *D) {
     if (!D) return DQGAN_EINVAL;
     if (D->d < 1 || D->ld < D->d || D->ld % 1024 != 0) return DQGAN_EINVAL;
-    if (D->ld / 1024 > INT32_MAX) return DQGAN_EINVAL;
+    if (D->ld / 256 > INT32_MAX) return DQGAN_EINVAL;  // the fused pass launches one workgroup per 256 columns
     if (D->M < 1 || D->M > 1024) return DQGAN_EINVAL;
     if (D->reserved != 0) return DQGAN_EINVAL;
     if (D->n_seg < 1 || (D->n_seg > 1 && !D->seg_offsets)) return DQGAN_EINVAL;

@@ -55,7 +55,7 @@ def _desc(**kw):
     dict(d=0), dict(ld=5000), dict(ld=4096), dict(M=0), dict(M=2000), dict(kind=9), dict(norm=2),
     dict(offs=[0, 1000, 4999]), dict(offs=[1, 1000, 5000]), dict(offs=[0, 1000, 1000]),
     dict(kind=1, norm=2, levels=7), dict(kind=1, norm=1, levels=15),
-    dict(kind=2, norm=0, k=0), dict(kind=2, norm=0, k=5001), dict(kind=3, norm=1),
+    dict(kind=2, norm=0, k=0), dict(kind=2, norm=0, k=5001), dict(kind=3, norm=1), dict(ld=1 << 40),
 ])
 def test_invalid_descriptors_rejected(lib, bad):
     from paper_2010_13359_amd import dqgan
