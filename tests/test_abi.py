@@ -79,3 +79,16 @@ def test_null_arguments(lib):
     assert lib.dqgan_wire_bytes(None, None, None, None, None, None) == dqgan.EINVAL
     assert lib.dqgan_step_scales(None, 0.1, None, None, ctypes.byref(w), None) == dqgan.EINVAL
     assert lib.dqgan_step_apply(None, 0.1, 0, None, None, None, None, ctypes.byref(w), None, None) == dqgan.EINVAL
+
+
+def test_pure_c_demo_compiles_and_links(tmp_path):
+    """include/dqgan.h is plain C: the demo builds with gcc -std=c11 -Werror
+    and links against libdqgan.so, the C oracle and the HIP runtime."""
+    import importlib.util
+    from oracle import oracle as orc
+    orc.lib()
+    spec = importlib.util.spec_from_file_location("c_abi_build", os.path.join(ROOT, "tests", "c_abi", "build.py"))
+    c_build = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(c_build)
+    out = c_build.build(str(tmp_path / "abi_demo"))
+    assert os.path.exists(out)
