@@ -288,7 +288,9 @@ def main():
     out["copy_ceiling"] = {"op": "torch.mul(g, 1.0, out=WX) over the step's own [M][ld] buffers (1 read, 1 write)",
                            "GB/s": round(cp_gbs, 1), "ms": round(cp_t, 4),
                            "roofline_frac_of_copy": round(achieved / cp_gbs, 4),
-                           "step_frac_of_copy": round(step_ach / cp_gbs, 4)}
+                           "step_frac_of_copy": round(step_ach / cp_gbs, 4),
+                           "step_counter_frac_of_copy": (round(step_counter / (ms_step * 1e-3) / 1e9 / cp_gbs, 4)
+                                                         if step_counter else None)}
     del graph
     plan.close()
     del Gs, E, W, WX, wire
