@@ -6,6 +6,8 @@ C2 (d = 6.3M, M = 16, s = 255) and C5 (the same shape, 8-bit Appendix A
 codes, infinity norm): every output against the oracle.
 C3 (d = 33.5M, M = 32, s = 15): sampled segments (the smallest, a middle one,
 the largest), all workers, element by element against the oracle.
+C2 and C5 also free-running over three iterations (each side on its own
+state, its own scales), every output against the oracle.
 C4 (d = 1e8, M = 64, top-k k = 1e6): sampled workers checked for the exact
 top-k property (ties to the lower index) from their p, residuals exact, and
 the server average / OMD outputs on sampled column windows against the
@@ -174,3 +176,64 @@ def test_c4_sampled_rows_and_windows():
         wx = np.stack([orc.extrapolate(eta, wt, Gs[m], Es[m]) for m in range(w.M)])
         assert_same("WX window %d" % a, WX[:, a:b].cpu().numpy(), wx)
     plan.close()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("index", [2, 5])
+def test_c2_c5_free_running(index):
+    """Three iterations at full size on each side's own state (gradients are
+    inputs, as in the benchmark).  Each side computes its own scales; they
+    agree within 1e-5 (binary64 sums in different orders, rounded once), so
+    a level can differ only at a near-tie of the rounding: such elements are
+    counted (at most 1 in 10^6 per step) and must differ by exactly one level
+    step in e_t; every other element of e_t, w_t and WX within 1e-5 relative
+    of the operand magnitude of its last operation."""
+    import torch
+    import synth
+    from oracle import oracle as orc
+    from paper_2010_13359_amd import dqgan
+    from gpu_common import rel_close, to_dev
+    w = synth.get(index)
+    print("C%d free-running" % index, flush=True)
+    d = w.d
+    E_r = np.zeros((w.M, w.ld), np.float32)
+    W_r = synth.init_params_np(w)
+    plan = dqgan.Plan.from_workload(w)
+    dev = torch.device("cuda:0")
+    E, W = to_dev(E_r), to_dev(W_r)
+    WX = torch.empty((w.M, w.ld), dtype=torch.float32, device=dev)
+    wire = plan.new_wire(dev)
+    eta = np.float32(w.eta)
+    k_levels = (1 << (w.levels - 1)) - 1 if w.kind == "mbit" else w.levels
+    ties = 0
+    for t in range(1, 4):
+        G = synth.gradients_np(w, t)
+        dqgan.step_fused(plan, w.eta, t, to_dev(G), E, W, WX, wire)
+        torch.cuda.synchronize()
+        P = np.abs(eta * G[:, :d]) + np.abs(E_r[:, :d])
+        W_prev = W_r[:d].copy()
+        ref = orc.step(w.as_dict(), eta, t, G, E_r, W_r)
+        gE, gW, gWX = E.cpu().numpy(), W.cpu().numpy(), WX.cpu().numpy()
+        scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
+        rel_close("scale", scales, ref["scale"], tau=1e-30)
+        bad = gE[:, :d] != ref["E"][:, :d]
+        n_bad = int(bad.sum())
+        assert n_bad <= 1e-6 * w.M * d, (t, n_bad)
+        if n_bad:
+            rows, cols = np.nonzero(bad)
+            seg = np.searchsorted(w.seg_offsets, cols, side="right") - 1
+            step = ref["scale"][rows, seg].astype(np.float64) / k_levels
+            diff = np.abs(gE[rows, cols].astype(np.float64) - ref["E"][rows, cols].astype(np.float64))
+            assert np.all(np.abs(diff - step) <= 1e-5 * step + 1e-30), (t, diff[:5], step[:5])
+        ties += n_bad
+        keep = ~bad
+        rel_close("E", np.where(keep, gE[:, :d], ref["E"][:, :d]), ref["E"][:, :d], tau=P + 1e-30)
+        X = np.abs(eta * G[:, :d]) + np.abs(E_r[:, :d])
+        # columns holding a near-tie carry its one-step difference into q-hat, w_t and WX
+        cols_ok = ~bad.any(axis=0)
+        rel_close("W", gW[:d][cols_ok], ref["W"][:d][cols_ok],
+                  tau=(np.abs(W_prev) + np.abs(ref["qhat"][:d]) + 1e-30)[cols_ok])
+        rel_close("WX", gWX[:, :d][:, cols_ok], ref["WX"][:, :d][:, cols_ok],
+                  tau=(np.abs(W_r[None, :d]) + X + 1e-30)[:, cols_ok])
+    plan.close()
+    print("near-tie level differences over 3 steps: %d" % ties)
