@@ -23,7 +23,9 @@
  *    padding of E and W is preserved, that of WX, P-hat and Q-hat is written
  *    as 0, and message bits beyond d are 0.
  *  - Every pointer is a device pointer (hipMalloc'd or equivalent), 16-byte
- *    aligned, owned by the caller, except those marked "host".
+ *    aligned, owned by the caller, except those marked "host".  The buffers
+ *    of one call must not overlap (E is updated in place; G, E, W, WX, Qhat,
+ *    P-hat and the message planes are distinct).
  *  - Arithmetic is IEEE binary32 with round-to-nearest-even, one rounding per
  *    operation, no fused multiply-add where the definitions below list
  *    separate operations; segment norms are summed in binary64 and rounded
@@ -198,8 +200,8 @@ dqgan_status dqgan_step_fused(dqgan_plan plan, float eta, uint32_t t, const floa
 /* The two passes of dqgan_step_fused, for callers that schedule or time them
  * separately.  dqgan_step_scales reads G and E (e_{t-1}) once and computes
  * what the compressor must know about the whole of each worker's vector
- * before it can encode any element: the segment scales (SIGN, QSGD; written
- * to out->scale) or the selection threshold (TOPK).  dqgan_step_apply then
+ * before it can encode any element: the segment scales (SIGN, QSGD, MBIT;
+ * written to out->scale) or the selection threshold (TOPK).  dqgan_step_apply then
  * runs the fused iteration with that state, which the plan holds in its
  * scratch: the two calls must be issued in this order on one stream with the
  * same G and E and no other call on the plan in between.  The arguments mean
