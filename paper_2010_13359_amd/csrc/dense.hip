@@ -258,15 +258,20 @@ __device__ __forceinline__ void store_topk(float *__restrict__ val_row, uint32_t
     uint32_t pre = 0;
 #pragma unroll
     for (int c = 0; c < 4; ++c) pre += __popcll(__ballot((mask >> c) & 1u) & below);
-#pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        if ((mask >> c) & 1u) {
-            const int64_t pos = static_cast<int64_t>(tile_base) + pre;
+    // Store round r writes each lane's r-th selected element: at a low
+    // selection density almost every wave needs one round (two store
+    // instructions) instead of one per element position of the quad.
+    const uint32_t n_sel = __popc(mask);
+    uint32_t rest = mask;
+    for (uint32_t r = 0; __ballot(r < n_sel) != 0; ++r) {
+        if (r < n_sel) {
+            const int c = __ffs(rest) - 1;
+            rest &= rest - 1;
+            const int64_t pos = static_cast<int64_t>(tile_base) + pre + r;
             if (pos < k) {
                 val_row[pos] = elem(cq.phat, c);
                 idx_row[pos] = static_cast<uint32_t>(i0 + c);
             }
-            ++pre;
         }
     }
 }
