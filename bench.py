@@ -153,7 +153,7 @@ def main():
                          "the per-pass times then come from an eager run of the same iterations")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
+        print("bench.py: the library runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
               "one batched matrix on a single device)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
