@@ -7,7 +7,8 @@ codes, infinity norm): every output against the oracle.
 C3 (d = 33.5M, M = 32, s = 15): sampled segments (the smallest, a middle one,
 the largest), all workers, element by element against the oracle.
 C2 and C5 also free-running over three iterations (each side on its own
-state, its own scales), every output against the oracle.
+state, its own scales), every output against the oracle; C3 and C6
+free-running on the sampled segments.
 C4 (d = 1e8, M = 64, top-k k = 1e6): sampled workers checked for the exact
 top-k property (ties to the lower index) from their p, residuals exact, and
 the server average / OMD outputs on sampled column windows against the
@@ -235,5 +236,80 @@ def test_c2_c5_free_running(index):
                   tau=(np.abs(W_prev) + np.abs(ref["qhat"][:d]) + 1e-30)[cols_ok])
         rel_close("WX", gWX[:, :d][:, cols_ok], ref["WX"][:, :d][:, cols_ok],
                   tau=(np.abs(W_r[None, :d]) + X + 1e-30)[:, cols_ok])
+    plan.close()
+    print("near-tie level differences over 3 steps: %d" % ties)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("index", [3, 6])
+def test_c3_c6_free_running_sampled_segments(index):
+    """Three iterations at full size in the launch configuration bench.py
+    times, each side on its own state.  Every quantity of the iteration is a
+    function of the columns of whole segments (scales per segment, the
+    average, update and evaluation point per column), so the oracle follows
+    the sampled segments (the smallest, a middle one, the largest) of all
+    workers on their own, with the global element index for the generator
+    counter.  Checks as in the C2/C5 free run: scales within 1e-5; e_t exact
+    except for counted near-ties of the rounding (one level step apart);
+    w_t and WX within 1e-5 relative of their last operation's operands."""
+    import torch
+    import synth
+    from oracle import oracle as orc
+    from paper_2010_13359_amd import dqgan
+    from gpu_common import rel_close
+    w = synth.get(index)
+    print("C%d free-running, sampled segments" % index, flush=True)
+    sizes = np.diff(w.seg_offsets)
+    picks = sorted({int(np.argmin(sizes)), int(np.argsort(sizes)[len(sizes) // 2]), int(np.argmax(sizes))})
+    dev = torch.device("cuda:0")
+    plan = dqgan.Plan.from_workload(w)
+    E = torch.zeros((w.M, w.ld), dtype=torch.float32, device=dev)
+    W = synth.init_params(w, device=dev)
+    WX = torch.empty((w.M, w.ld), dtype=torch.float32, device=dev)
+    wire = plan.new_wire(dev)
+    eta = np.float32(w.eta)
+    k_levels = (1 << (w.levels - 1)) - 1 if w.kind == "mbit" else w.levels
+    seg = {j: (w.seg_offsets[j], w.seg_offsets[j + 1]) for j in picks}
+    E_r = {j: np.zeros((w.M, b - a), np.float32) for j, (a, b) in seg.items()}
+    W_r = {j: W[a:b].cpu().numpy() for j, (a, b) in seg.items()}
+    G = None
+    ties = 0
+    for t in range(1, 4):
+        G = synth.gradients(w, t, device=dev, out=G)
+        dqgan.step_scales(plan, w.eta, G, E, wire)
+        dqgan.step_apply(plan, w.eta, t, G, E, W, WX, wire)
+        torch.cuda.synchronize()
+        scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
+        for j, (a, b) in seg.items():
+            n = b - a
+            Gs = G[:, a:b].cpu().numpy()
+            own = np.empty(w.M, np.float32)
+            phat = np.empty((w.M, n), np.float32)
+            enew = np.empty((w.M, n), np.float32)
+            for m in range(w.M):
+                p = orc.ef_accumulate(eta, Gs[m], E_r[j][m])
+                own[m] = orc.scale(p, w.norm)
+                _, _, phat[m], enew[m] = orc.qsgd_encode(p, own[m], k_levels, w.quant_seed, m, t, i0=a)
+            rel_close("scale seg %d step %d" % (j, t), scales[:, j], own, tau=1e-30)
+            wt = orc.omd_update(orc.aggregate(phat, n), W_r[j])
+            wx = np.stack([orc.extrapolate(eta, wt, Gs[m], enew[m]) for m in range(w.M)])
+            gE, gW, gWX = E[:, a:b].cpu().numpy(), W[a:b].cpu().numpy(), WX[:, a:b].cpu().numpy()
+            bad = gE != enew
+            n_bad = int(bad.sum())
+            assert n_bad <= max(1, 1e-6 * w.M * n), (j, t, n_bad)
+            if n_bad:
+                rows, _ = np.nonzero(bad)
+                step = own[rows].astype(np.float64) / k_levels
+                diff = np.abs(gE[bad].astype(np.float64) - enew[bad].astype(np.float64))
+                assert np.all(np.abs(diff - step) <= 1e-5 * step + 1e-30), (j, t, diff[:5], step[:5])
+            ties += n_bad
+            X = np.abs(eta * Gs) + np.abs(enew)
+            cols_ok = ~bad.any(axis=0)
+            rel_close("W seg %d step %d" % (j, t), gW[cols_ok], wt[cols_ok],
+                      tau=(np.abs(W_r[j]) + np.abs(wt - W_r[j]) + 1e-30)[cols_ok])
+            rel_close("WX seg %d step %d" % (j, t), gWX[:, cols_ok], wx[:, cols_ok],
+                      tau=(np.abs(wt[None, :]) + X + 1e-30)[:, cols_ok])
+            E_r[j], W_r[j] = enew, wt
+        print("step %d done" % t, flush=True)
     plan.close()
     print("near-tie level differences over 3 steps: %d" % ties)
