@@ -98,8 +98,7 @@ typedef struct {
     int32_t levels;               /* QSGD s: 255 (8-bit level field) or 15 (4-bit);
                                      MBIT: code bits m, 8 or 4 (k = 127 or 7)      */
     int32_t reserved;             /* must be 0                                      */
-    int64_t k;                    /* TOPK: 1 <= k <= d, d < 2^32, M <= 64
-                                     (larger M: DQGAN_EUNSUPPORTED)                 */
+    int64_t k;                    /* TOPK: 1 <= k <= d, d < 2^32                    */
     uint64_t seed;                /* QSGD, MBIT: key of the Philox4x32-10 generator */
 } dqgan_desc;
 

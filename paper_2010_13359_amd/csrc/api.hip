@@ -59,7 +59,6 @@ dqgan_status validate_desc(const dqgan_desc *D) {
         case DQGAN_TOPK:
             if (D->norm != DQGAN_NORM_NONE) return DQGAN_EINVAL;
             if (D->k < 1 || D->k > D->d || D->d >= (int64_t(1) << 32)) return DQGAN_EINVAL;
-            if (D->M > 64) return DQGAN_EUNSUPPORTED;
             break;
         case DQGAN_IDENTITY:
             if (D->norm != DQGAN_NORM_NONE) return DQGAN_EINVAL;

@@ -375,9 +375,12 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
                                                   float *__restrict__ Qhat, uint32_t *__restrict__ sign_plane,
                                                   uint32_t *__restrict__ level_plane, float *__restrict__ val,
                                                   const float2 *__restrict__ consts, const int64_t *__restrict__ off,
-                                                  const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
+                                                  const int32_t *__restrict__ tile_seg, RowArgs a, float invM,
+                                                  TopkArgs ta) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
     const int64_t i0 = 4 * q;
+    // top-k: each wave's 64 quads are one counting tile
+    const int64_t tile = static_cast<int64_t>(blockIdx.x) * (kQuadsPerBlock / 64) + (threadIdx.x >> 6);
     const int M = MT > 0 ? MT : a.M;
     constexpr int kUnroll = MT > 0 ? MT : 1;
     int js[4];
@@ -389,11 +392,21 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
         const int64_t rb = static_cast<int64_t>(m) * a.ld;
         const f32x4 g = ld_stream(G + rb + i0);
         const f32x4 e = ld_stream(E + rb + i0);
-        const QuadCodes cq = encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg,
-                                               a.s, a.k0, a.k1, a.t);
+        QuadCodes cq;
+        if constexpr (KIND == kTopk) {
+            const TopkRow *rw = ta.rows + m;
+            cq = encode_quad_topk(g, e, a.eta, i0, a.d, rw->T, rw->I);
+        } else {
+            cq = encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg, a.s, a.k0,
+                                   a.k1, a.t);
+        }
         st_stream(E + rb + i0, cq.enew);
-        store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq,
-                                   a.stream_msg != 0);
+        if constexpr (KIND == kTopk) {
+            store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + tile], i0, cq);
+        } else {
+            store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq,
+                                       a.stream_msg != 0);
+        }
         if (m == 0) {
             acc = cq.phat;
         } else {
@@ -748,11 +761,25 @@ RowArgs row_args(const dqgan_plan_s &P, float eta, uint32_t t) {
 // else 0 (the kernels divide).
 float inv_m(int M) { return (M & (M - 1)) == 0 ? 1.0f / static_cast<float>(M) : 0.0f; }
 
+// The state the top-k apply pass reads (threshold per row, tile offsets).
+TopkArgs topk_args(const dqgan_plan_s &P, const dqgan_wire &w) {
+    TopkArgs ta{};
+    if (P.desc.kind == kTopk) {
+        ta.rows = P.topk.rows;
+        ta.tile_off = P.topk.tile_off;
+        ta.n_tiles = P.topk.n_tiles;
+        ta.k = P.desc.k;
+        ta.idx = w.idx;
+    }
+    return ta;
+}
+
 template <int KIND, int LB, int MT>
 hipError_t fused_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                         const dqgan_wire &w, float *Qhat, hipStream_t st) {
     hipLaunchKernelGGL((k_fused<KIND, LB, MT>), dim3(static_cast<unsigned>(P.n_tiles)), dim3(kBlock), 0, st, G, E, W,
-                       WX, Qhat, w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a, inv_m(P.desc.M));
+                       WX, Qhat, w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a, inv_m(P.desc.M),
+                       topk_args(P, w));
     return hipGetLastError();
 }
 
@@ -760,14 +787,7 @@ template <int KIND, int LB, int R, int NG>
 hipError_t split_launch(const dqgan_plan_s &P, const RowArgs &a, const float *G, float *E, float *W, float *WX,
                         const dqgan_wire &w, float *Qhat, hipStream_t st) {
     if (P.desc.M > R * NG) return hipErrorInvalidValue;  // every worker must belong to a wave
-    TopkArgs ta{};
-    if (KIND == kTopk) {
-        ta.rows = P.topk.rows;
-        ta.tile_off = P.topk.tile_off;
-        ta.n_tiles = P.topk.n_tiles;
-        ta.k = P.desc.k;
-        ta.idx = w.idx;
-    }
+    const TopkArgs ta = topk_args(P, w);
     const dim3 grid(static_cast<unsigned>(P.n_tiles * 4)), block(64 * NG);
     // Only 8-bit planes have a second store kind (store_fields32).
     constexpr bool kTwoKinds = (KIND == kQsgd || KIND == kMbit) && LB == 8;
@@ -798,12 +818,8 @@ hipError_t fused_by_m(const dqgan_plan_s &P, const RowArgs &a, const float *G, f
     if (M <= 16) return split_launch<KIND, LB, 2, 8>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 32) return split_launch<KIND, LB, 4, 8>(P, a, G, E, W, WX, w, Qhat, st);
     if (M <= 64) return split_launch<KIND, LB, 4, 16>(P, a, G, E, W, WX, w, Qhat, st);
-    if constexpr (KIND == kTopk) {
-        return hipErrorNotSupported;  // top-k plans are limited to M <= 64
-    } else {
-        if (M <= 128) return split_launch<KIND, LB, 8, 16>(P, a, G, E, W, WX, w, Qhat, st);
-        return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
-    }
+    if (M <= 128) return split_launch<KIND, LB, 8, 16>(P, a, G, E, W, WX, w, Qhat, st);
+    return fused_launch<KIND, LB, 0>(P, a, G, E, W, WX, w, Qhat, st);
 }
 
 }  // namespace

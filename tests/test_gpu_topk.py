@@ -1,8 +1,9 @@
 """GPU parity of the top-k compressor (Theorem 1; ties to the lower index)
 through the C ABI, against the oracle on the same inputs.  Indices and
 values of the message, residuals, the average and the OMD outputs must be
-identical.  Shapes cover the sampled-band path (Gaussian and Laplace data)
-and the full-row fallback (heavy ties, all-zero rows, k = d)."""
+identical.  Shapes cover the sampled-band path (Gaussian and Laplace data),
+the full-row fallback (heavy ties, all-zero rows, k = d) and every launch
+shape of the apply pass (up to 300 workers)."""
 import numpy as np
 import pytest
 
@@ -41,11 +42,22 @@ def _case(name):
         return custom(d=200000, M=2, kind="topk", k=500, eta=1e-2, seed=32), "cluster"
     if name == "m16_d1000000_k10000":
         return custom(d=1000000, M=16, kind="topk", k=10000, eta=1e-3, seed=29), None
+    # more than 64 workers: 16 waves x 8 rows (65..128), then one lane
+    # walking every row (129..1024)
+    if name == "m65_d20000_k200":
+        return custom(d=20000, M=65, kind="topk", k=200, eta=1e-2, seed=33), None
+    if name == "m128_d9000_k90":
+        return custom(d=9000, M=128, kind="topk", k=90, eta=1e-2, seed=34, law="laplace"), None
+    if name == "m130_d7001_k70":
+        return custom(d=7001, M=130, kind="topk", k=70, eta=1e-2, seed=35), None
+    if name == "m300_d3000_k3000":
+        return custom(d=3000, M=300, kind="topk", k=3000, eta=1e-2, seed=36), None
     raise KeyError(name)
 
 
 NAMES = ["m4_d5000_k50", "m8_d200000_k2000", "m5_d3001_k7", "m64_d300000_k3000", "m3_d1_k1", "m2_d4096_kd",
-         "m4_ties", "m4_ties_big", "m4_zero_rows", "m2_hidden_cluster", "m16_d1000000_k10000"]
+         "m4_ties", "m4_ties_big", "m4_zero_rows", "m2_hidden_cluster", "m16_d1000000_k10000", "m65_d20000_k200",
+         "m128_d9000_k90", "m130_d7001_k70", "m300_d3000_k3000"]
 
 
 def _inputs(name):
