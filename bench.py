@@ -94,6 +94,38 @@ def workload_label(w):
     return "C%d %s: d=%d, M=%d workers, %s, %s, eta=%g" % (w.index, w.name, w.d, w.M, comp, scope, w.eta)
 
 
+def separate_calls(plan, w, G, E, W, WX, wire, dev, reps=5):
+    """The worker and server sides as separate calls (what a multi-process
+    deployment would run): dqgan_compress_ef (both passes), dqgan_aggregate
+    and dqgan_omd_step, each timed with HIP events after the step's timed
+    region, with the algorithmic bytes of each call's one pass."""
+    import torch
+    from paper_2010_13359_amd import dqgan
+    Q = torch.empty(w.ld, dtype=torch.float32, device=dev)
+    msg = w.M * w.d * wire_bits(w) / 8.0
+    scales = 4.0 * w.M * w.n_seg if w.kind in ("sign", "qsgd", "mbit") else 0.0
+    calls = {
+        "compress_ef": (lambda: dqgan.compress_ef(plan, w.eta, 1, G, E, None, wire),
+                        12.0 * w.M * w.d + msg + scales),
+        "aggregate": (lambda: dqgan.aggregate(plan, wire, Q), msg + scales + 4.0 * w.d),
+        "omd_step": (lambda: dqgan.omd_step(plan, w.eta, Q, W, G, E, WX), 12.0 * w.M * w.d + 12.0 * w.d),
+    }
+    res = {}
+    for name, (fn, alg) in calls.items():
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
+        res[name] = {"ms": round(ms, 4), "algorithmic_GB/s": round(alg / (ms * 1e-3) / 1e9, 1)}
+    del Q
+    return res
+
+
 def traffic_record(kernel_key, group):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     if it was taken on the current kernel sources; else None."""
@@ -291,6 +323,7 @@ def main():
                            "step_frac_of_copy": round(step_ach / cp_gbs, 4),
                            "step_counter_frac_of_copy": (round(step_counter / (ms_step * 1e-3) / 1e9 / cp_gbs, 4)
                                                          if step_counter else None)}
+    out["separate_calls"] = separate_calls(plan, w, Gs[0], E, W, WX, wire, dev)
     del graph
     plan.close()
     del Gs, E, W, WX, wire

@@ -344,7 +344,11 @@ struct RowArgs {
     int32_t stream_msg;               // message planes larger than the Infinity Cache: streaming stores
 };
 
-// Worker side only (dqgan_compress_ef): one (quad, worker) per thread.
+// Worker side only (dqgan_compress_ef): one quad per thread for kEncRows
+// consecutive workers, whose g and e are all loaded before the first is
+// encoded (more loads in flight per lane).
+constexpr int kEncRows = 4;
+
 template <int KIND, int LB>
 __global__ __launch_bounds__(kBlock) void k_encode_rows(const float *__restrict__ G, float *__restrict__ E,
                                                         uint32_t *__restrict__ sign_plane,
@@ -353,18 +357,41 @@ __global__ __launch_bounds__(kBlock) void k_encode_rows(const float *__restrict_
                                                         const int64_t *__restrict__ off,
                                                         const int32_t *__restrict__ tile_seg, RowArgs a) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
-    const int m = blockIdx.y;
+    const int m0 = static_cast<int>(blockIdx.y) * kEncRows;
     const int64_t i0 = 4 * q;
-    const int64_t rb = static_cast<int64_t>(m) * a.ld;
     int js[4];
     lookup_segments(off, tile_seg, i0, a.d, js);
-    const f32x4 g = ld_stream(G + rb + i0);
-    const f32x4 e = ld_stream(E + rb + i0);
-    const QuadCodes cq =
-        encode_quad<KIND>(g, e, a.eta, i0, a.d, m, js, consts + static_cast<int64_t>(m) * a.n_seg, a.s, a.k0, a.k1, a.t);
-    st_stream(E + rb + i0, cq.enew);
-    store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq,
-                               a.stream_msg != 0);
+    const int j_first = __builtin_amdgcn_readfirstlane(js[0]);
+    const bool one_seg = __ballot(js[0] != j_first || js[3] != j_first) == 0;
+    const int z[4] = {0, 0, 0, 0};
+    f32x4 gv[kEncRows], ev[kEncRows];
+#pragma unroll
+    for (int u = 0; u < kEncRows; ++u) {
+        const int m = m0 + u;
+        if (m < a.M) {
+            const int64_t rb = static_cast<int64_t>(m) * a.ld;
+            gv[u] = ld_stream(G + rb + i0);
+            ev[u] = ld_stream(E + rb + i0);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kEncRows; ++u) {
+        const int m = m0 + u;
+        if (m < a.M) {
+            const int64_t rb = static_cast<int64_t>(m) * a.ld;
+            const float2 *crow = consts + static_cast<int64_t>(m) * a.n_seg;
+            QuadCodes cq;
+            if (one_seg) {
+                const float2 c1[1] = {crow[j_first]};
+                cq = encode_quad<KIND>(gv[u], ev[u], a.eta, i0, a.d, m, z, c1, a.s, a.k0, a.k1, a.t);
+            } else {
+                cq = encode_quad<KIND>(gv[u], ev[u], a.eta, i0, a.d, m, js, crow, a.s, a.k0, a.k1, a.t);
+            }
+            st_stream(E + rb + i0, cq.enew);
+            store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q,
+                                       cq, a.stream_msg != 0);
+        }
+    }
 }
 
 // The fused step.  MT > 0: M == MT, the extrapolation operands stay in
@@ -572,45 +599,35 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
     }
 }
 
-// Decode one quad of one row's message to p-hat.
-template <int KIND, int LB>
-__device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_row, const uint32_t *__restrict__ level_row,
-                                             const float *__restrict__ val_row, const float2 *__restrict__ crow,
-                                             int64_t q, int64_t d, const int js[4]) {
-    const int64_t i0 = 4 * q;
+// Decode one quad of one row's message to p-hat from its fields: nib = the
+// four sign bits (SIGN, QSGD), raw = the quad's level or code bits (QSGD,
+// MBIT: 32 bits for 8-bit fields, the low 16 for 4-bit fields).
+// CHECK_D: elements at or beyond d decode to 0 (only the last quads of a
+// row need it).  The magnitude is never negative, so the sign bit is set by
+// OR (-0 for a zero level with the sign bit set, as the encoder gives).
+template <int KIND, int LB, bool CHECK_D = true>
+__device__ __forceinline__ f32x4 decode_fields(uint32_t nib, uint32_t raw, const float2 *__restrict__ crow,
+                                               const int js[4], int64_t i0, int64_t d) {
     f32x4 out = {0.0f, 0.0f, 0.0f, 0.0f};
-    if (KIND == kIdentity) {
-        const f32x4 v = ld4(val_row + i0);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) set_elem(out, c, (i0 + c < d) ? elem(v, c) : 0.0f);
-        return out;
-    }
-    uint32_t nib = 0u, lev = 0u;
+    uint32_t lev = 0u;
     if (KIND == kMbit) {
         if (LB == 8) {
-            const uint32_t wv = level_row[q];
-            lev = wv & 0x7F7F7F7Fu;
-            nib = ((wv >> 7) & 1u) | ((wv >> 14) & 2u) | ((wv >> 21) & 4u) | ((wv >> 28) & 8u);
+            lev = raw & 0x7F7F7F7Fu;
+            nib = ((raw >> 7) & 1u) | ((raw >> 14) & 2u) | ((raw >> 21) & 4u) | ((raw >> 28) & 8u);
         } else {
-            const uint32_t h = reinterpret_cast<const uint16_t *>(level_row)[q];
-            lev = (h & 0x7u) | ((h & 0x70u) << 4) | ((h & 0x700u) << 8) | ((h & 0x7000u) << 12);
-            nib = ((h >> 3) & 1u) | ((h >> 6) & 2u) | ((h >> 9) & 4u) | ((h >> 12) & 8u);
+            lev = (raw & 0x7u) | ((raw & 0x70u) << 4) | ((raw & 0x700u) << 8) | ((raw & 0x7000u) << 12);
+            nib = ((raw >> 3) & 1u) | ((raw >> 6) & 2u) | ((raw >> 9) & 4u) | ((raw >> 12) & 8u);
         }
-    } else {
-        nib = (sign_row[q >> 3] >> (4 * (q & 7))) & 0xFu;
     }
     if (KIND == kQsgd) {
-        if (LB == 8) {
-            lev = level_row[q];
-        } else {
-            const uint32_t h = reinterpret_cast<const uint16_t *>(level_row)[q];
-            lev = (h & 0xFu) | ((h & 0xF0u) << 4) | ((h & 0xF00u) << 8) | ((h & 0xF000u) << 12);
-        }
+        if (LB == 8)
+            lev = raw;
+        else
+            lev = (raw & 0xFu) | ((raw & 0xF0u) << 4) | ((raw & 0xF00u) << 8) | ((raw & 0xF000u) << 12);
     }
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-        if (i0 + c >= d) continue;
-        const bool neg = (nib >> c) & 1u;
+        if (CHECK_D && i0 + c >= d) continue;
         float mag;
         if (KIND == kSign) {
             mag = crow[js[c]].x;
@@ -618,9 +635,29 @@ __device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_r
             const uint32_t l = (lev >> (8 * c)) & 0xFFu;
             mag = mul_rn(static_cast<float>(l), crow[js[c]].y);
         }
-        set_elem(out, c, neg ? -mag : mag);
+        set_elem(out, c, __uint_as_float(__float_as_uint(mag) | (((nib >> c) & 1u) << 31)));
     }
     return out;
+}
+
+// Decode one quad of one row's message to p-hat.
+template <int KIND, int LB>
+__device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_row, const uint32_t *__restrict__ level_row,
+                                             const float *__restrict__ val_row, const float2 *__restrict__ crow,
+                                             int64_t q, int64_t d, const int js[4]) {
+    const int64_t i0 = 4 * q;
+    if (KIND == kIdentity) {
+        const f32x4 v = ld4(val_row + i0);
+        f32x4 out;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) set_elem(out, c, (i0 + c < d) ? elem(v, c) : 0.0f);
+        return out;
+    }
+    const uint32_t nib = (KIND == kSign || KIND == kQsgd) ? (sign_row[q >> 3] >> (4 * (q & 7))) & 0xFu : 0u;
+    uint32_t raw = 0u;
+    if (KIND == kQsgd || KIND == kMbit)
+        raw = LB == 8 ? level_row[q] : static_cast<uint32_t>(reinterpret_cast<const uint16_t *>(level_row)[q]);
+    return decode_fields<KIND, LB>(nib, raw, crow, js, i0, d);
 }
 
 template <int KIND, int LB>
@@ -639,6 +676,14 @@ __global__ __launch_bounds__(kBlock) void k_unpack(const uint32_t *__restrict__ 
     st_stream(Phat + rb + 4 * q, v);
 }
 
+// Server average of the M messages.  A thread covers four consecutive
+// quads (16 elements: 16 sign bits, 8 or 16 bytes of fields per row, so
+// each row's loads are 2-16 bytes per lane rather than sub-word), and takes
+// the rows in chunks of kAggRows whose fields are all loaded before the
+// first is decoded; the sum runs in ascending worker order.
+constexpr int kAggQuads = 4;
+constexpr int kAggRows = 4;
+
 template <int KIND, int LB>
 __global__ __launch_bounds__(kBlock) void k_aggregate(const uint32_t *__restrict__ sign_plane,
                                                       const uint32_t *__restrict__ level_plane,
@@ -646,29 +691,110 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(const uint32_t *__restrict
                                                       const float2 *__restrict__ consts,
                                                       const int64_t *__restrict__ off,
                                                       const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
-    const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
-    int js[4];
-    lookup_segments(off, tile_seg, 4 * q, a.d, js);
-    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-    for (int m = 0; m < a.M; ++m) {
-        const int64_t rb = static_cast<int64_t>(m) * a.ld;
-        const f32x4 v = decode_quad<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb,
-                                              consts + static_cast<int64_t>(m) * a.n_seg, q, a.d, js);
-        if (m == 0) {
-            acc = v;
-        } else {
+    const int64_t g16 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;  // group of 16 elements
+    const int64_t q0 = kAggQuads * g16;
+    const bool live = 4 * q0 < a.ld;
+    int js[kAggQuads][4];
 #pragma unroll
-            for (int c = 0; c < 4; ++c) set_elem(acc, c, add_rn(elem(acc, c), elem(v, c)));
+    for (int k = 0; k < kAggQuads; ++k) lookup_segments(off, tile_seg, live ? 4 * (q0 + k) : 0, a.d, js[k]);
+    // the whole wave in one segment (the common case): one scalar load of
+    // the constants per row
+    const int j_first = __builtin_amdgcn_readfirstlane(js[0][0]);
+    const bool one_seg = __ballot(live && (js[0][0] != j_first || js[kAggQuads - 1][3] != j_first)) == 0;
+    const int z[4] = {0, 0, 0, 0};
+    // every element of the wave below d: no per-element bound tests
+    const bool full = __ballot(4 * (q0 + kAggQuads) > a.d) == 0;
+    constexpr int kFieldWords = (KIND == kQsgd || KIND == kMbit) ? LB / 2 : 0;  // 32-bit words of fields per row
+    f32x4 acc[kAggQuads];
+#pragma unroll
+    for (int k = 0; k < kAggQuads; ++k) acc[k] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+    // the fields of row m for this thread's 16 elements
+    auto load_row = [&](int m, uint32_t &sg, uint32_t (&fw)[kFieldWords > 0 ? kFieldWords : 1],
+                        f32x4 (&vv)[KIND == kIdentity ? kAggQuads : 1]) {
+        if (KIND == kSign || KIND == kQsgd) sg = reinterpret_cast<const uint16_t *>(sign_plane + m * a.sign_words)[g16];
+        if (kFieldWords == 4) {
+            const u32x4 v = *reinterpret_cast<const u32x4 *>(level_plane + m * a.level_words + 4 * g16);
+            fw[0] = v.x;
+            fw[kFieldWords > 1 ? 1 : 0] = v.y;
+            fw[kFieldWords > 2 ? 2 : 0] = v.z;
+            fw[kFieldWords > 3 ? 3 : 0] = v.w;
+        } else if (kFieldWords == 2) {
+            const uint2 v = *reinterpret_cast<const uint2 *>(level_plane + m * a.level_words + 2 * g16);
+            fw[0] = v.x;
+            fw[kFieldWords > 1 ? 1 : 0] = v.y;
+        }
+        if (KIND == kIdentity) {
+#pragma unroll
+            for (int k = 0; k < kAggQuads; ++k)
+                vv[KIND == kIdentity ? k : 0] = ld4(val + static_cast<int64_t>(m) * a.ld + 4 * (q0 + k));
+        }
+    };
+    // add row m (ascending order) given its loaded fields and its constants
+    auto add_row = [&](int m, uint32_t sg, const uint32_t (&fw)[kFieldWords > 0 ? kFieldWords : 1],
+                       const f32x4 (&vv)[KIND == kIdentity ? kAggQuads : 1], const float2 *crow, bool uniform) {
+#pragma unroll
+        for (int k = 0; k < kAggQuads; ++k) {
+            const int64_t i0 = 4 * (q0 + k);
+            f32x4 v;
+            if (KIND == kIdentity) {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) set_elem(v, c, (i0 + c < a.d) ? elem(vv[KIND == kIdentity ? k : 0], c) : 0.0f);
+            } else {
+                const uint32_t nib = (KIND == kSign || KIND == kQsgd) ? (sg >> (4 * k)) & 0xFu : 0u;
+                uint32_t raw = 0u;
+                if (kFieldWords == 4) raw = fw[k < kFieldWords ? k : 0];
+                if (kFieldWords == 2) raw = (fw[(k >> 1) < kFieldWords ? (k >> 1) : 0] >> (16 * (k & 1))) & 0xFFFFu;
+                v = full ? decode_fields<KIND, LB, false>(nib, raw, crow, uniform ? z : js[k], i0, a.d)
+                         : decode_fields<KIND, LB, true>(nib, raw, crow, uniform ? z : js[k], i0, a.d);
+            }
+            if (m == 0) {
+                acc[k] = v;
+            } else {
+#pragma unroll
+                for (int c = 0; c < 4; ++c) set_elem(acc[k], c, add_rn(elem(acc[k], c), elem(v, c)));
+            }
+        }
+    };
+    if (one_seg) {
+        // kAggRows rows' fields loaded before the first is decoded
+        for (int m0 = 0; m0 < a.M; m0 += kAggRows) {
+            uint32_t sg[kAggRows];
+            uint32_t fw[kAggRows][kFieldWords > 0 ? kFieldWords : 1];
+            f32x4 vv[kAggRows][KIND == kIdentity ? kAggQuads : 1];
+#pragma unroll
+            for (int u = 0; u < kAggRows; ++u)
+                if (m0 + u < a.M && live) load_row(m0 + u, sg[u], fw[u], vv[u]);
+#pragma unroll
+            for (int u = 0; u < kAggRows; ++u) {
+                const int m = m0 + u;
+                if (m < a.M && live) {
+                    const float2 c1[1] = {consts[static_cast<int64_t>(m) * a.n_seg + j_first]};
+                    add_row(m, sg[u], fw[u], vv[u], c1, true);
+                }
+            }
+        }
+    } else if (live) {
+        // a wave across segment boundaries: one row at a time
+        for (int m = 0; m < a.M; ++m) {
+            uint32_t sg = 0u;
+            uint32_t fw[kFieldWords > 0 ? kFieldWords : 1];
+            f32x4 vv[KIND == kIdentity ? kAggQuads : 1];
+            load_row(m, sg, fw, vv);
+            add_row(m, sg, fw, vv, consts + static_cast<int64_t>(m) * a.n_seg, false);
         }
     }
-    f32x4 qh;
+    if (!live) return;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-        const float sacc = elem(acc, c);
-        set_elem(qh, c, invM > 0.0f ? mul_rn(sacc, invM)
-                                    : static_cast<float>(static_cast<double>(sacc) / static_cast<double>(a.M)));
+    for (int k = 0; k < kAggQuads; ++k) {
+        f32x4 qh;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const float sacc = elem(acc[k], c);
+            set_elem(qh, c, invM > 0.0f ? mul_rn(sacc, invM)
+                                        : static_cast<float>(static_cast<double>(sacc) / static_cast<double>(a.M)));
+        }
+        st4(Qhat + 4 * (q0 + k), qh);
     }
-    st4(Qhat + 4 * q, qh);
 }
 
 __global__ __launch_bounds__(kBlock) void k_omd(const float *__restrict__ Qhat, float *__restrict__ W,
@@ -856,7 +982,7 @@ hipError_t launch_consts_from_scales(const dqgan_plan_s &P, const float *scales,
 hipError_t launch_encode(const dqgan_plan_s &P, float eta, uint32_t t, const float *G, float *E, const dqgan_wire &w,
                          hipStream_t st) {
     const RowArgs a = row_args(P, eta, t);
-    const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
+    const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>((P.desc.M + kEncRows - 1) / kEncRows));
     const int kind = P.desc.kind;
     if (kind == kSign)
         hipLaunchKernelGGL((k_encode_rows<kSign, 0>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
@@ -938,7 +1064,7 @@ hipError_t launch_unpack_dense(const dqgan_plan_s &P, const dqgan_wire &w, float
 
 hipError_t launch_aggregate_dense(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st) {
     const RowArgs a = row_args(P, 0.0f, 0);
-    const dim3 grid(static_cast<unsigned>(P.n_tiles));
+    const dim3 grid(static_cast<unsigned>((P.n_tiles + kAggQuads - 1) / kAggQuads));  // 16 elements per thread
     const int kind = P.desc.kind;
     const float im = inv_m(P.desc.M);
     if (kind != kIdentity) {
