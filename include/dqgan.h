@@ -116,7 +116,10 @@ typedef struct dqgan_plan_s *dqgan_plan;
  * Scales (SIGN, QSGD, MBIT): fp32 [M][n_seg], the scale (SIGN) or sigma
  *   (QSGD, MBIT) of segment j of worker m.
  * val/idx (TOPK): fp32 and uint32 [M][k]; the selected p_i and their indices
- *   i, in ascending i.  (IDENTITY: val is the dense fp32 [M][ld] p-hat = p.)
+ *   i, in ascending i, each below d.  A message that breaks this (read by
+ *   dqgan_unpack or dqgan_aggregate) gives undefined values but no access
+ *   outside the buffers: indices at or beyond d are skipped.
+ *   (IDENTITY: val is the dense fp32 [M][ld] p-hat = p.)
  * Unused planes may be NULL. */
 typedef struct {
     uint32_t *sign;

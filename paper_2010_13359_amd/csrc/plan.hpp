@@ -53,6 +53,8 @@ struct TopkScratch {
     uint32_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per 256-element tile
     uint32_t *tile_off = nullptr;   // [M][n_tiles] exclusive prefix of tile_cnt
     uint32_t *chunk_sum = nullptr;  // [M][n_scan_chunks] tile counts per scan chunk
+    uint32_t *agg_start = nullptr;  // [M][n_agg_tiles + 1] first message entry per server-average tile
+    int64_t n_agg_tiles = 0;
     int64_t n_tiles = 0;
     int64_t n_chunks = 0;           // sampled chunks per row
     uint32_t n_samples = 0;         // sampled elements per row

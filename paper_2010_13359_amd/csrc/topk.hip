@@ -665,29 +665,183 @@ __global__ __launch_bounds__(1024) void k_topk_scan_add(TopkRow *__restrict__ ro
         if (t0 + j < n_tiles) orow[t0 + j] += b;
 }
 
-// Server side: scatter the messages (unpack), or add them in worker order.
+// Server side: scatter the messages to the dense p-hat (unpack); indices at
+// or beyond d (only a malformed message has them) are skipped.
 __global__ __launch_bounds__(kBlock) void k_topk_scatter(const float *__restrict__ val, const uint32_t *__restrict__ idx,
-                                                         int64_t k, float *__restrict__ out, int64_t ld) {
+                                                         int64_t k, int64_t d, float *__restrict__ out, int64_t ld) {
     const int m = blockIdx.y;
     for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < k;
-         j += static_cast<int64_t>(gridDim.x) * kBlock)
-        out[static_cast<int64_t>(m) * ld + idx[static_cast<int64_t>(m) * k + j]] = val[static_cast<int64_t>(m) * k + j];
-}
-
-__global__ __launch_bounds__(kBlock) void k_topk_scatter_add(const float *__restrict__ val,
-                                                             const uint32_t *__restrict__ idx, int64_t k,
-                                                             float *__restrict__ S) {
-    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < k;
          j += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const uint32_t i = idx[j];
-        S[i] = add_rn(S[i], val[j]);
+        const uint32_t i = idx[static_cast<int64_t>(m) * k + j];
+        if (i < d) out[static_cast<int64_t>(m) * ld + i] = val[static_cast<int64_t>(m) * k + j];
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_divide(float *__restrict__ S, int64_t n, int32_t M, float invM) {
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
-         i += static_cast<int64_t>(gridDim.x) * kBlock)
-        S[i] = invM > 0.0f ? mul_rn(S[i], invM) : static_cast<float>(static_cast<double>(S[i]) / static_cast<double>(M));
+// Server average of the M top-k messages by column tiles.  Each worker's
+// list is sorted by index, so its entries in tile T are one run
+// [start(m, T), start(m, T+1)).  A workgroup stages the runs of all workers
+// in LDS; each thread then adds the entries of its own columns worker by
+// worker, so every column's sum is the ascending-worker sum from 0 the
+// definition gives; the tile is written once.  A tile with more entries
+// than the stage holds adds the runs from memory, worker by worker with a
+// barrier between workers.  Indices outside the tile (only a malformed
+// message has them) are skipped.
+constexpr int kAggTile = 2048;   // columns per workgroup
+constexpr int kAggStage = 2048;  // message entries staged per workgroup (32 KiB of LDS in all)
+
+// start(m, T) = the first entry j of worker m with idx[j] >= T * kAggTile,
+// for T = 0 .. n_t (k for the tiles past the last entry).  A wave takes
+// kStartsPer * 64 consecutive entries in coalesced rounds (round u: entry
+// u * 64 + lane), all loaded before the first is examined; the previous
+// entry's index comes from the neighbouring lane.
+constexpr int kStartsPer = 16;
+
+__global__ __launch_bounds__(kBlock) void k_topk_agg_starts(const uint32_t *__restrict__ idx, int64_t k, int64_t n_t,
+                                                            uint32_t *__restrict__ start) {
+    const int m = blockIdx.y;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t *row = idx + static_cast<int64_t>(m) * k;
+    uint32_t *srow = start + static_cast<int64_t>(m) * (n_t + 1);
+    const int64_t jw = (static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave) * (64 * kStartsPer);
+    if (jw > k) return;
+    uint32_t v[kStartsPer];
+#pragma unroll
+    for (int u = 0; u < kStartsPer; ++u) {
+        const int64_t j = jw + 64 * u + lane;
+        v[u] = j < k ? row[j] : 0u;
+    }
+    const uint32_t before = jw > 0 ? row[jw - 1] : 0u;  // the entry before the wave's first
+    uint32_t last_prev_round = before;
+#pragma unroll
+    for (int u = 0; u < kStartsPer; ++u) {
+        const int64_t j = jw + 64 * u + lane;
+        const uint32_t up = __shfl_up(v[u], 1);
+        const uint32_t prev_idx = lane > 0 ? up : last_prev_round;
+        last_prev_round = __shfl(v[u], 63);
+        if (j > k) continue;
+        const int64_t tj = j < k ? min(static_cast<int64_t>(v[u] / kAggTile), n_t) : n_t;
+        const int64_t tp = j > 0 ? min(static_cast<int64_t>(prev_idx / kAggTile), n_t) : -1;
+        for (int64_t T = tp + 1; T <= tj; ++T) srow[T] = static_cast<uint32_t>(j);
+    }
+}
+
+static_assert(kAggTile % kBlock == 0, "each thread owns the same number of columns of a tile");
+constexpr int kAggMaxM = 1024;            // the library's largest worker count
+constexpr int kAggPerThread = kAggMaxM / kBlock;  // workers per thread in the run scan
+
+__global__ __launch_bounds__(kBlock) void k_topk_agg_tiles(const float *__restrict__ val,
+                                                           const uint32_t *__restrict__ idx, int64_t k, int32_t M,
+                                                           const uint32_t *__restrict__ start, int64_t n_t,
+                                                           int64_t d, int64_t ld, float *__restrict__ Qhat,
+                                                           float invM) {
+    __shared__ float acc[kAggTile];
+    __shared__ uint32_t st_col[kAggStage];
+    __shared__ float st_val[kAggStage];
+    __shared__ uint32_t run_s[kAggMaxM];     // first entry of each worker's run
+    __shared__ uint32_t woff[kAggMaxM + 1];  // staged offset of each worker's run
+    __shared__ uint32_t wsum[kBlock / 64];
+    const int64_t T = blockIdx.x;
+    const int64_t base = T * kAggTile;
+    const int tid = threadIdx.x;
+    for (int c = tid; c < kAggTile; c += kBlock) acc[c] = 0.0f;
+    // runs of workers kAggPerThread*tid ...: clamped to [0, k]
+    uint32_t rs[kAggPerThread], rn[kAggPerThread], mine = 0;
+#pragma unroll
+    for (int u = 0; u < kAggPerThread; ++u) {
+        const int m = kAggPerThread * tid + u;
+        rs[u] = 0u;
+        rn[u] = 0u;
+        if (m < M) {
+            const uint32_t *srow = start + static_cast<int64_t>(m) * (n_t + 1);
+            const int64_t s = min(static_cast<int64_t>(srow[T]), k);
+            const int64_t e = min(static_cast<int64_t>(srow[T + 1]), k);
+            rs[u] = static_cast<uint32_t>(s);
+            rn[u] = e > s ? static_cast<uint32_t>(e - s) : 0u;
+        }
+        mine += rn[u];
+    }
+    // exclusive scan of the per-thread counts over the workgroup
+    const int lane = tid & 63, wave = tid >> 6;
+    uint32_t incl = mine;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_up(incl, o);
+        if (lane >= o) incl += x;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t o = incl - mine, total = 0;
+    for (int w = 0; w < kBlock / 64; ++w) {
+        if (w < wave) o += wsum[w];
+        total += wsum[w];
+    }
+#pragma unroll
+    for (int u = 0; u < kAggPerThread; ++u) {
+        const int m = kAggPerThread * tid + u;
+        if (m < M) {
+            run_s[m] = rs[u];
+            woff[m] = o;
+        }
+        o += rn[u];
+    }
+    if (tid == 0) woff[M] = total;
+    __syncthreads();
+    if (total <= kAggStage) {
+        // stage every run: staged entry g belongs to the last worker whose
+        // offset is <= g (binary search over the offsets)
+        for (uint32_t g = tid; g < total; g += kBlock) {
+            int lo = 0, hi = M - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (woff[mid] <= g) lo = mid;
+                else hi = mid - 1;
+            }
+            const int64_t j = static_cast<int64_t>(run_s[lo]) + (g - woff[lo]);
+            st_col[g] = idx[static_cast<int64_t>(lo) * k + j];
+            st_val[g] = val[static_cast<int64_t>(lo) * k + j];
+        }
+        __syncthreads();
+        // Thread tid owns columns [8 tid, 8 tid + 8) of the tile and adds
+        // their entries worker by worker in ascending order: a binary search
+        // finds each worker's first entry at or beyond the thread's first
+        // column, and the worker's run is sorted, so no barrier is needed.
+        const int64_t c0 = static_cast<int64_t>(kAggTile / kBlock) * tid;
+        for (int m = 0; m < M; ++m) {
+            uint32_t lo = woff[m], hi = woff[m + 1];
+            const uint32_t end = hi;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi) >> 1;
+                if (static_cast<int64_t>(st_col[mid]) < base + c0) lo = mid + 1;
+                else hi = mid;
+            }
+            for (uint32_t j = lo; j < end; ++j) {
+                const int64_t c = static_cast<int64_t>(st_col[j]) - base - c0;
+                if (c >= kAggTile / kBlock) break;
+                if (c >= 0) acc[c0 + c] = add_rn(acc[c0 + c], st_val[j]);
+            }
+        }
+        __syncthreads();
+    } else {
+        // a dense tile: the runs straight from memory, worker by worker
+        for (int m = 0; m < M; ++m) {
+            const int64_t s = run_s[m], n = woff[m + 1] - woff[m];
+            const float *vrow = val + static_cast<int64_t>(m) * k;
+            const uint32_t *irow = idx + static_cast<int64_t>(m) * k;
+            for (int64_t j = tid; j < n; j += kBlock) {
+                const int64_t c = static_cast<int64_t>(irow[s + j]) - base;
+                if (c >= 0 && c < kAggTile) acc[c] = add_rn(acc[c], vrow[s + j]);
+            }
+            __syncthreads();
+        }
+    }
+    for (int c = tid; c < kAggTile; c += kBlock) {
+        const int64_t i = base + c;
+        if (i >= ld) break;
+        const float sacc = acc[c];
+        Qhat[i] = i >= d ? 0.0f
+                         : invM > 0.0f ? mul_rn(sacc, invM)
+                                       : static_cast<float>(static_cast<double>(sacc) / static_cast<double>(M));
+    }
 }
 
 unsigned grid_for(int64_t n, int64_t cap_blocks = 65536) {
@@ -722,6 +876,10 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
     const int64_t nsc = (S.n_tiles + kScanChunk - 1) / kScanChunk;
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.chunk_sum), M * static_cast<size_t>(nsc) * sizeof(uint32_t));
+    S.n_agg_tiles = (D.ld + kAggTile - 1) / kAggTile;
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.agg_start),
+                      M * static_cast<size_t>(S.n_agg_tiles + 1) * sizeof(uint32_t));
     return e;
 }
 
@@ -733,6 +891,7 @@ void topk_free(dqgan_plan_s &P) {
     (void)hipFree(S.tile_cnt);
     (void)hipFree(S.tile_off);
     (void)hipFree(S.chunk_sum);
+    (void)hipFree(S.agg_start);
     S = TopkScratch{};
 }
 
@@ -778,18 +937,20 @@ hipError_t launch_topk_unpack(const dqgan_plan_s &P, const dqgan_wire &w, float 
     const int64_t n = static_cast<int64_t>(D.M) * D.ld;
     hipLaunchKernelGGL(k_fill_f32, dim3(grid_for(n)), dim3(kBlock), 0, st, Phat, n);
     hipLaunchKernelGGL(k_topk_scatter, dim3(grid_for(D.k, 4096), static_cast<unsigned>(D.M)), dim3(kBlock), 0, st,
-                       w.val, w.idx, D.k, Phat, D.ld);
+                       w.val, w.idx, D.k, D.d, Phat, D.ld);
     return hipGetLastError();
 }
 
 hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st) {
     const dqgan_desc &D = P.desc;
-    hipLaunchKernelGGL(k_fill_f32, dim3(grid_for(D.ld)), dim3(kBlock), 0, st, Qhat, D.ld);
-    for (int m = 0; m < D.M; ++m)
-        hipLaunchKernelGGL(k_topk_scatter_add, dim3(grid_for(D.k, 4096)), dim3(kBlock), 0, st,
-                           w.val + static_cast<int64_t>(m) * D.k, w.idx + static_cast<int64_t>(m) * D.k, D.k, Qhat);
+    const TopkScratch &S = P.topk;
+    const int64_t per_block = static_cast<int64_t>(kBlock) * kStartsPer;
+    const int64_t sb = (D.k + 1 + per_block - 1) / per_block;
+    hipLaunchKernelGGL(k_topk_agg_starts, dim3(static_cast<unsigned>(sb), static_cast<unsigned>(D.M)), dim3(kBlock), 0,
+                       st, w.idx, D.k, S.n_agg_tiles, S.agg_start);
     const float im = (D.M & (D.M - 1)) == 0 ? 1.0f / static_cast<float>(D.M) : 0.0f;
-    hipLaunchKernelGGL(k_divide, dim3(grid_for(D.d)), dim3(kBlock), 0, st, Qhat, D.d, D.M, im);
+    hipLaunchKernelGGL(k_topk_agg_tiles, dim3(static_cast<unsigned>(S.n_agg_tiles)), dim3(kBlock), 0, st, w.val, w.idx,
+                       D.k, D.M, S.agg_start, S.n_agg_tiles, D.d, D.ld, Qhat, im);
     return hipGetLastError();
 }
 
