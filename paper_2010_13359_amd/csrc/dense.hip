@@ -16,6 +16,8 @@
 //      w_t = w_{t-1} - q-hat; every wave then writes its rows' evaluation
 //      points w_t - (fl(eta g) + e_t).  k_fused (one lane walks all M rows)
 //      serves M > 128.
+#include <type_traits>
+
 #include "device.hpp"
 #include "plan.hpp"
 
@@ -979,117 +981,85 @@ hipError_t launch_consts_from_scales(const dqgan_plan_s &P, const float *scales,
     return launch_segment_scales(P, 0.0f, nullptr, nullptr, scales, nullptr, st);
 }
 
+namespace {
+
+// Calls f(kind, field bits) with both as compile-time constants, for the
+// dense compressors: (SIGN, 0), (QSGD, 8 or 4), (MBIT, 8 or 4), (IDENTITY, 0).
+template <int V>
+using Const = std::integral_constant<int, V>;
+
+template <typename F>
+hipError_t with_dense_kind(const dqgan_plan_s &P, F &&f) {
+    switch (P.desc.kind) {
+        case kSign: return f(Const<kSign>{}, Const<0>{});
+        case kQsgd: return P.level_bits == 8 ? f(Const<kQsgd>{}, Const<8>{}) : f(Const<kQsgd>{}, Const<4>{});
+        case kMbit: return P.level_bits == 8 ? f(Const<kMbit>{}, Const<8>{}) : f(Const<kMbit>{}, Const<4>{});
+        default: return f(Const<kIdentity>{}, Const<0>{});
+    }
+}
+
+}  // namespace
+
 hipError_t launch_encode(const dqgan_plan_s &P, float eta, uint32_t t, const float *G, float *E, const dqgan_wire &w,
                          hipStream_t st) {
     const RowArgs a = row_args(P, eta, t);
     const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>((P.desc.M + kEncRows - 1) / kEncRows));
-    const int kind = P.desc.kind;
-    if (kind == kSign)
-        hipLaunchKernelGGL((k_encode_rows<kSign, 0>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    else if (kind == kQsgd && P.level_bits == 8)
-        hipLaunchKernelGGL((k_encode_rows<kQsgd, 8>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    else if (kind == kQsgd)
-        hipLaunchKernelGGL((k_encode_rows<kQsgd, 4>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    else if (kind == kMbit && P.level_bits == 8)
-        hipLaunchKernelGGL((k_encode_rows<kMbit, 8>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    else if (kind == kMbit)
-        hipLaunchKernelGGL((k_encode_rows<kMbit, 4>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    else
-        hipLaunchKernelGGL((k_encode_rows<kIdentity, 0>), grid, dim3(kBlock), 0, st, G, E, w.sign, w.level, w.val,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    return hipGetLastError();
+    return with_dense_kind(P, [&](auto K, auto L) {
+        hipLaunchKernelGGL((k_encode_rows<decltype(K)::value, decltype(L)::value>), grid, dim3(kBlock), 0, st, G, E,
+                           w.sign, w.level, w.val, P.d_consts, P.d_off, P.d_tile_seg, a);
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_fused_dense(const dqgan_plan_s &P, float eta, uint32_t t, const float *G, float *E, float *W,
                               float *WX, const dqgan_wire &w, float *Qhat, hipStream_t st) {
     const RowArgs a = row_args(P, eta, t);
-    const int kind = P.desc.kind;
-    if (kind == kSign) return fused_by_m<kSign, 0>(P, a, G, E, W, WX, w, Qhat, st);
-    if (kind == kQsgd && P.level_bits == 8) return fused_by_m<kQsgd, 8>(P, a, G, E, W, WX, w, Qhat, st);
-    if (kind == kQsgd) return fused_by_m<kQsgd, 4>(P, a, G, E, W, WX, w, Qhat, st);
-    if (kind == kMbit && P.level_bits == 8) return fused_by_m<kMbit, 8>(P, a, G, E, W, WX, w, Qhat, st);
-    if (kind == kMbit) return fused_by_m<kMbit, 4>(P, a, G, E, W, WX, w, Qhat, st);
-    return fused_by_m<kIdentity, 0>(P, a, G, E, W, WX, w, Qhat, st);
+    return with_dense_kind(P, [&](auto K, auto L) {
+        return fused_by_m<decltype(K)::value, decltype(L)::value>(P, a, G, E, W, WX, w, Qhat, st);
+    });
 }
 
 hipError_t launch_pack(const dqgan_plan_s &P, const uint16_t *codes, const dqgan_wire &w, hipStream_t st) {
     const RowArgs a = row_args(P, 0.0f, 0);
     const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
-    if (P.desc.kind == kSign)
-        hipLaunchKernelGGL((k_pack<0, kSign>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
-    else if (P.desc.kind == kMbit && P.level_bits == 8)
-        hipLaunchKernelGGL((k_pack<8, kMbit>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
-    else if (P.desc.kind == kMbit)
-        hipLaunchKernelGGL((k_pack<4, kMbit>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
-    else if (P.level_bits == 8)
-        hipLaunchKernelGGL((k_pack<8, kQsgd>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
-    else
-        hipLaunchKernelGGL((k_pack<4, kQsgd>), grid, dim3(kBlock), 0, st, codes, w.sign, w.level, a);
-    return hipGetLastError();
+    return with_dense_kind(P, [&](auto K, auto L) {
+        if constexpr (decltype(K)::value == kIdentity) {
+            return hipErrorInvalidValue;  // the identity has no codes to pack
+        } else {
+            hipLaunchKernelGGL((k_pack<decltype(L)::value, decltype(K)::value>), grid, dim3(kBlock), 0, st, codes,
+                               w.sign, w.level, a);
+            return hipGetLastError();
+        }
+    });
 }
 
 hipError_t launch_unpack_dense(const dqgan_plan_s &P, const dqgan_wire &w, float *Phat, hipStream_t st) {
     const RowArgs a = row_args(P, 0.0f, 0);
     const dim3 grid(static_cast<unsigned>(P.n_tiles), static_cast<unsigned>(P.desc.M));
-    const int kind = P.desc.kind;
-    if (kind != kIdentity) {
+    if (P.desc.kind != kIdentity) {
         hipError_t err = launch_consts_from_scales(P, w.scale, st);
         if (err != hipSuccess) return err;
     }
-    if (kind == kSign)
-        hipLaunchKernelGGL((k_unpack<kSign, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
-                           P.d_off, P.d_tile_seg, a);
-    else if (kind == kQsgd && P.level_bits == 8)
-        hipLaunchKernelGGL((k_unpack<kQsgd, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
-                           P.d_off, P.d_tile_seg, a);
-    else if (kind == kQsgd)
-        hipLaunchKernelGGL((k_unpack<kQsgd, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
-                           P.d_off, P.d_tile_seg, a);
-    else if (kind == kMbit && P.level_bits == 8)
-        hipLaunchKernelGGL((k_unpack<kMbit, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
-                           P.d_off, P.d_tile_seg, a);
-    else if (kind == kMbit)
-        hipLaunchKernelGGL((k_unpack<kMbit, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat, P.d_consts,
-                           P.d_off, P.d_tile_seg, a);
-    else
-        hipLaunchKernelGGL((k_unpack<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Phat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a);
-    return hipGetLastError();
+    return with_dense_kind(P, [&](auto K, auto L) {
+        hipLaunchKernelGGL((k_unpack<decltype(K)::value, decltype(L)::value>), grid, dim3(kBlock), 0, st, w.sign,
+                           w.level, w.val, Phat, P.d_consts, P.d_off, P.d_tile_seg, a);
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_aggregate_dense(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st) {
     const RowArgs a = row_args(P, 0.0f, 0);
     const dim3 grid(static_cast<unsigned>((P.n_tiles + kAggQuads - 1) / kAggQuads));  // 16 elements per thread
-    const int kind = P.desc.kind;
     const float im = inv_m(P.desc.M);
-    if (kind != kIdentity) {
+    if (P.desc.kind != kIdentity) {
         hipError_t err = launch_consts_from_scales(P, w.scale, st);
         if (err != hipSuccess) return err;
     }
-    if (kind == kSign)
-        hipLaunchKernelGGL((k_aggregate<kSign, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
-    else if (kind == kQsgd && P.level_bits == 8)
-        hipLaunchKernelGGL((k_aggregate<kQsgd, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
-    else if (kind == kQsgd)
-        hipLaunchKernelGGL((k_aggregate<kQsgd, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
-    else if (kind == kMbit && P.level_bits == 8)
-        hipLaunchKernelGGL((k_aggregate<kMbit, 8>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
-    else if (kind == kMbit)
-        hipLaunchKernelGGL((k_aggregate<kMbit, 4>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
-    else
-        hipLaunchKernelGGL((k_aggregate<kIdentity, 0>), grid, dim3(kBlock), 0, st, w.sign, w.level, w.val, Qhat,
-                           P.d_consts, P.d_off, P.d_tile_seg, a, im);
-    return hipGetLastError();
+    return with_dense_kind(P, [&](auto K, auto L) {
+        hipLaunchKernelGGL((k_aggregate<decltype(K)::value, decltype(L)::value>), grid, dim3(kBlock), 0, st, w.sign,
+                           w.level, w.val, Qhat, P.d_consts, P.d_off, P.d_tile_seg, a, im);
+        return hipGetLastError();
+    });
 }
 
 hipError_t launch_topk_apply(const dqgan_plan_s &P, float eta, const float *G, float *E, float *W, float *WX,
