@@ -47,6 +47,9 @@ CASES = {
     "qsgd15_m65_split8": lambda: custom(d=3000, M=65, kind="qsgd", levels=15, eta=1e-2, seed=18),
     "sign_m128_split8": lambda: custom(d=2100, M=128, kind="sign", seg_offsets=[0, 100, 2100], eta=1e-2, seed=26),
     "mbit4_m100_split8": lambda: custom(d=1500, M=100, kind="mbit", levels=4, norm="linf", eta=1e-2, seed=27),
+    # the largest worker count the library takes
+    "sign_m1024_max": lambda: custom(d=1100, M=1024, kind="sign", seg_offsets=[0, 37, 1100], eta=1e-2, seed=29),
+    "mbit4_m1024_d1": lambda: custom(d=1, M=1024, kind="mbit", levels=4, norm="linf", eta=1e-2, seed=30),
     "qsgd255_m130_one_lane": lambda: custom(d=1800, M=130, kind="qsgd", levels=255, seg_offsets=[0, 901, 1800],
                                             eta=1e-2, seed=28),
     "mbit8_linf_m4": lambda: custom(d=5000, M=4, kind="mbit", levels=8, norm="linf", seg_offsets=[0, 1234, 5000],

@@ -52,12 +52,14 @@ def _case(name):
         return custom(d=7001, M=130, kind="topk", k=70, eta=1e-2, seed=35), None
     if name == "m300_d3000_k3000":
         return custom(d=3000, M=300, kind="topk", k=3000, eta=1e-2, seed=36), None
+    if name == "m1024_d2500_k25":
+        return custom(d=2500, M=1024, kind="topk", k=25, eta=1e-2, seed=37), None
     raise KeyError(name)
 
 
 NAMES = ["m4_d5000_k50", "m8_d200000_k2000", "m5_d3001_k7", "m64_d300000_k3000", "m3_d1_k1", "m2_d4096_kd",
          "m4_ties", "m4_ties_big", "m4_zero_rows", "m2_hidden_cluster", "m16_d1000000_k10000", "m65_d20000_k200",
-         "m128_d9000_k90", "m130_d7001_k70", "m300_d3000_k3000"]
+         "m128_d9000_k90", "m130_d7001_k70", "m300_d3000_k3000", "m1024_d2500_k25"]
 
 
 def _inputs(name):
