@@ -168,12 +168,15 @@ dqgan_status dqgan_plan_create(const dqgan_desc *desc, dqgan_plan *out) {
             tile_seg[static_cast<size_t>(tl)] = j;
         }
     }
+    const int64_t piece = static_cast<int64_t>(desc->M) * (d / dq::kPieceElems) >= dq::kPieceBlocksForLong
+                              ? dq::kPieceElems
+                              : dq::kPieceElems / 2;
     std::vector<Piece> pieces;
     std::vector<int32_t> seg_piece(static_cast<size_t>(S) + 1);
     for (int32_t j = 0; j < S; ++j) {
         seg_piece[static_cast<size_t>(j)] = static_cast<int32_t>(pieces.size());
-        for (int64_t a = P->offsets[j]; a < P->offsets[j + 1]; a += dq::kPieceElems) {
-            const int64_t b = a + dq::kPieceElems < P->offsets[j + 1] ? a + dq::kPieceElems : P->offsets[j + 1];
+        for (int64_t a = P->offsets[j]; a < P->offsets[j + 1]; a += piece) {
+            const int64_t b = a + piece < P->offsets[j + 1] ? a + piece : P->offsets[j + 1];
             pieces.push_back(Piece{a, static_cast<int32_t>(b - a), j});
         }
     }
