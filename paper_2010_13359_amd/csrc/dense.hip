@@ -298,8 +298,17 @@ template <int KIND, int LB, bool STREAM>
 __device__ __forceinline__ void store_message(uint32_t *__restrict__ sign_row, uint32_t *__restrict__ level_row,
                                               float *__restrict__ val_row, int64_t q, const QuadCodes &cq) {
     if (KIND == kSign || KIND == kQsgd) {
+        // the word of each 8-lane group (32 elements), then the four words of
+        // lanes 4, 12, 20, 28 (and 36 .. 60) gathered into one 16-byte store:
+        // 0.5 % faster than eight 4-byte stores (32 workers x 2^25 elements
+        // and 16 x 6.3M); as a non-temporal store 3 % slower
         const uint32_t word = or_reduce8_to_lane4(cq.sign_nib << (4 * (q & 7)));
-        if ((q & 7) == 4) sign_row[q >> 3] = word;
+        u32x4 v4;
+        v4.x = word;
+        v4.y = static_cast<uint32_t>(__shfl_down(static_cast<int>(word), 8));
+        v4.z = static_cast<uint32_t>(__shfl_down(static_cast<int>(word), 16));
+        v4.w = static_cast<uint32_t>(__shfl_down(static_cast<int>(word), 24));
+        if ((q & 31) == 4) *reinterpret_cast<u32x4 *>(sign_row + (q >> 3)) = v4;
     }
     if (KIND == kQsgd) {
         if (LB == 8) {
