@@ -820,17 +820,30 @@ __global__ __launch_bounds__(kBlock) void k_omd(const float *__restrict__ Qhat, 
     for (int c = 0; c < 4; ++c) set_elem(wt, c, (i0 + c < d) ? sub_rn(elem(w, c), elem(qh, c)) : elem(w, c));
     st4(W + i0, wt);
     if (!WX) return;
-    for (int m = 0; m < M; ++m) {
-        const int64_t rb = static_cast<int64_t>(m) * ld;
-        const f32x4 g = ld_stream(G + rb + i0);
-        const f32x4 e = ld_stream(E + rb + i0);
-        f32x4 wx;
+    // kOmdRows workers' g and e loaded before the first evaluation point
+    constexpr int kOmdRows = 4;
+    for (int m0 = 0; m0 < M; m0 += kOmdRows) {
+        f32x4 gv[kOmdRows], ev[kOmdRows];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            const float x = add_rn(mul_rn(eta, elem(g, c)), elem(e, c));
-            set_elem(wx, c, (i0 + c < d) ? sub_rn(elem(wt, c), x) : 0.0f);
+        for (int u = 0; u < kOmdRows; ++u) {
+            if (m0 + u < M) {
+                const int64_t rb = static_cast<int64_t>(m0 + u) * ld;
+                gv[u] = ld_stream(G + rb + i0);
+                ev[u] = ld_stream(E + rb + i0);
+            }
         }
-        st_stream(WX + rb + i0, wx);
+#pragma unroll
+        for (int u = 0; u < kOmdRows; ++u) {
+            if (m0 + u < M) {
+                f32x4 wx;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const float x = add_rn(mul_rn(eta, elem(gv[u], c)), elem(ev[u], c));
+                    set_elem(wx, c, (i0 + c < d) ? sub_rn(elem(wt, c), x) : 0.0f);
+                }
+                st_stream(WX + static_cast<int64_t>(m0 + u) * ld + i0, wx);
+            }
+        }
     }
 }
 
