@@ -24,9 +24,14 @@
  *   - s-level stochastic quantizer: r = fl(|p| * fl(s/sigma)),
  *     l = min(floor(r), s), frac = r - l, round up iff u < frac, level capped
  *     at s; the decoded value is copysign(fl(level * fl(sigma/s)), p).
- *     A zero-norm segment quantizes to level 0 everywhere, and so does a
- *     zero element (|v_i| / ||v|| = 0 gives l = 0 and round-up probability 0,
- *     even where s/sigma overflows).
+ *     For sigma < 2^-64 both |p| and sigma are first multiplied by 2^64
+ *     (exact) and the decoded magnitude by 2^-64 (one rounding), so that
+ *     fl(s/sigma) cannot overflow and fl(sigma/s) keeps its significand;
+ *     wherever the plain evaluation stays in the normal range the two give
+ *     the same bits.  A segment whose norm is 0 or not finite (a norm that
+ *     the binary32 scale of the message cannot hold) quantizes to level 0
+ *     everywhere, and so does a zero element (|v_i| / ||v|| = 0 gives l = 0
+ *     and round-up probability 0).
  *   - Uniforms for stochastic rounding come from Philox4x32-10 with key
  *     (lo32(seed), hi32(seed)) and counter (lo32(i>>2), m, t, hi32(i>>2));
  *     element i takes output word (i & 3) and u = (word >> 8) * 2^-24.
@@ -35,6 +40,7 @@
  *   - Aggregation sums the M decoded messages in ascending worker order in
  *     binary32 and divides the sum by M once.
  */
+#include <float.h>
 #include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -129,6 +135,25 @@ void oracle_sign_encode(int64_t n, const float *p, float scale, uint8_t *bits, f
     }
 }
 
+/* The range in which equation (qsgd) is evaluated for a segment of norm
+ * sigma.  r = |v_i| s / sigma does not change when v is scaled, but
+ * fl(s/sigma) overflows binary32 once sigma < s / FLT_MAX and fl(sigma/s)
+ * drops significand bits once it is subnormal.  For sigma < 2^-64 the
+ * magnitudes and the norm are multiplied by up = 2^64 (exact: every |v_i| is
+ * at most about sigma) and the decoded magnitude by down = 2^-64.  Returns 0
+ * for a norm of 0 or one that is not finite: nothing of the segment is sent. */
+static int qsgd_range(float sigma, float *up, float *down) {
+    if (!(sigma > 0.0f) || !(sigma <= FLT_MAX)) return 0;
+    if (sigma < 0x1.0p-64f) {
+        *up = 0x1.0p64f;
+        *down = 0x1.0p-64f;
+    } else {
+        *up = 1.0f;
+        *down = 1.0f;
+    }
+    return 1;
+}
+
 /* s-level stochastic quantizer (equation qsgd): for the segment starting at
  * row index i0, xi_i = l/s or (l+1)/s with P[(l+1)/s] = |p_i| s / sigma - l.
  * levels[i] receives the integer level, bits[i] the sign bit. */
@@ -136,17 +161,19 @@ void oracle_qsgd_encode(int64_t n, int64_t i0, const float *p, float sigma, int3
                         uint64_t seed, int32_t m, uint32_t t,
                         uint8_t *bits, uint16_t *levels, float *phat, float *e_out) {
     float fs = (float)s;
-    float inv = 0.0f, step = 0.0f;
-    if (sigma > 0.0f) {
-        inv = fs / sigma;
-        step = sigma / fs;
+    float up = 1.0f, down = 1.0f, inv = 0.0f, step = 0.0f;
+    int live = qsgd_range(sigma, &up, &down);
+    if (live) {
+        float su = sigma * up;
+        inv = fs / su;
+        step = su / fs;
     }
     for (int64_t i = 0; i < n; ++i) {
         int neg = signbit(p[i]) ? 1 : 0;
         int32_t level = 0;
         float a = fabsf(p[i]);
-        if (sigma > 0.0f && a > 0.0f) {
-            float r = a * inv;
+        if (live && a > 0.0f) {
+            float r = (a * up) * inv;
             float l = floorf(r);
             if (l > fs) l = fs;
             float frac = (l == fs) ? 0.0f : r - l;
@@ -154,7 +181,7 @@ void oracle_qsgd_encode(int64_t n, int64_t i0, const float *p, float sigma, int3
             level = (int32_t)l + ((u < frac) ? 1 : 0);
             if (level > s) level = s;
         }
-        float mag = (float)level * step;
+        float mag = ((float)level * step) * down;
         float q = copysignf(mag, p[i]);
         bits[i] = (uint8_t)neg;
         levels[i] = (uint16_t)level;
@@ -237,13 +264,13 @@ void oracle_unpack_bits(int64_t n, int32_t b, const uint32_t *words, uint16_t *f
  * after pulling it).  kind 0 = scaled sign, 1 = s-level quantizer. */
 void oracle_decode_segment(int32_t kind, int64_t n, const uint16_t *signs, const uint16_t *levels,
                            float scale, int32_t s, float *phat) {
-    float step = 0.0f;
-    if (kind == 1 && scale > 0.0f) step = scale / (float)s;
+    float up = 1.0f, down = 1.0f, step = 0.0f;
+    if (kind == 1 && qsgd_range(scale, &up, &down)) step = (scale * up) / (float)s;
     for (int64_t i = 0; i < n; ++i) {
         if (kind == 0) {
             phat[i] = signs[i] ? -scale : scale;
         } else {
-            float mag = (float)levels[i] * step;
+            float mag = ((float)levels[i] * step) * down;
             phat[i] = signs[i] ? -mag : mag;
         }
     }

@@ -49,7 +49,15 @@ MUTATIONS = [
     ("qsgd_nearest", "deterministic nearest level before the random step",
      [("float l = floorf(r);", "float l = rintf(r);")]),
     ("qsgd_step_reciprocal", "decode step as the reciprocal of s / sigma",
-     [("step = sigma / fs;", "step = 1.0f / inv;")]),
+     [("step = su / fs;", "step = 1.0f / inv;")]),
+    ("qsgd_no_range", "s / sigma evaluated unscaled for tiny norms (overflows: every level s)",
+     [("if (sigma < 0x1.0p-64f) {", "if (sigma < 0.0f) {")]),
+    ("qsgd_inf_norm", "a norm of +inf quantized like a finite one (p-hat = 0 * inf)",
+     [("if (!(sigma > 0.0f) || !(sigma <= FLT_MAX)) return 0;", "if (!(sigma > 0.0f)) return 0;")]),
+    ("qsgd_range_not_undone", "tiny-norm p-hat left in the scaled range",
+     [("float mag = ((float)level * step) * down;", "float mag = (float)level * step;")]),
+    ("decode_range_not_undone", "server decodes tiny-norm levels without scaling back",
+     [("float mag = ((float)levels[i] * step) * down;", "float mag = (float)levels[i] * step;")]),
     ("qsgd_segment_counter", "every segment restarts the random counter at 0",
      [("oracle_qsgd_encode(n, a, p + a, sc, D->levels,", "oracle_qsgd_encode(n, 0, p + a, sc, D->levels,")]),
     ("philox_word", "uniform from the wrong output word",
@@ -79,8 +87,8 @@ MUTATIONS = [
     ("decode_sign_flip", "server decodes the sign plane reversed",
      [("phat[i] = signs[i] ? -scale : scale;", "phat[i] = signs[i] ? scale : -scale;")]),
     ("decode_step", "server decodes levels with s + 1 steps",
-     [("if (kind == 1 && scale > 0.0f) step = scale / (float)s;",
-       "if (kind == 1 && scale > 0.0f) step = scale / (float)(s + 1);")]),
+     [("if (kind == 1 && qsgd_range(scale, &up, &down)) step = (scale * up) / (float)s;",
+       "if (kind == 1 && qsgd_range(scale, &up, &down)) step = (scale * up) / (float)(s + 1);")]),
     ("mbit_split_mask", "m-bit split keeps the sign bit in the level",
      [("uint16_t mask = (uint16_t)((1u << (mbits - 1)) - 1u);", "uint16_t mask = (uint16_t)((1u << mbits) - 1u);")]),
     ("linf_flag_ignored", "the quantizer ignores the max-norm flag",
