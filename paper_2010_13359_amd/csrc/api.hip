@@ -197,7 +197,7 @@ dqgan_status dqgan_plan_create(const dqgan_desc *desc, dqgan_plan *out) {
         e = hipMalloc(reinterpret_cast<void **>(&P->d_partial), npart * sizeof(double));
         if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&P->d_pmax), npart * sizeof(float));
         if (e == hipSuccess)
-            e = hipMalloc(reinterpret_cast<void **>(&P->d_consts), static_cast<size_t>(desc->M) * S * sizeof(float2));
+            e = hipMalloc(reinterpret_cast<void **>(&P->d_consts), static_cast<size_t>(desc->M) * S * sizeof(dq::SegConst));
     }
     if (e == hipSuccess && desc->kind == DQGAN_TOPK) e = dq::topk_alloc(*P);
     if (e != hipSuccess) {

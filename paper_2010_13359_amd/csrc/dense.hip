@@ -98,8 +98,9 @@ __global__ __launch_bounds__(kBlock) void k_segment_partials(const float *__rest
 }
 
 // Combine the partials of each (worker, segment) in piece order, or take the
-// caller's scales, and derive the per-segment constants: SIGN (scale, -);
-// QSGD (fl(s/sigma), fl(sigma/s)), (0, 0) for sigma = 0.  Quotients of two
+// caller's scales, and derive the per-segment constants (SegConst): SIGN the
+// scale; QSGD, MBIT fl(s/(u sigma)) and fl(u sigma/s), negated when u = 2^64
+// (sigma < 2^-64), zeros for sigma = 0 or not finite.  Quotients of two
 // binary32 values computed in binary64 and rounded to binary32 equal the
 // correctly rounded binary32 quotient (53 >= 2*24 + 2).
 __global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int levels, const double *__restrict__ partial,
@@ -107,7 +108,7 @@ __global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int lev
                                                      const int32_t *__restrict__ seg_piece,
                                                      const int64_t *__restrict__ off, int32_t M, int32_t n_seg,
                                                      const float *__restrict__ scales_in, float *__restrict__ scale_out,
-                                                     float2 *__restrict__ consts) {
+                                                     SegConst *__restrict__ consts) {
     // One wave per (worker, segment): lane l adds the segment's pieces
     // l, l+64, ... in order, then a fixed butterfly combines the lanes.
     const int64_t tid = (static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x) >> 6;
@@ -138,21 +139,33 @@ __global__ __launch_bounds__(kBlock) void k_finalize(int kind, int norm, int lev
     }
     if (lane != 0) return;
     if (scale_out) scale_out[tid] = sc;
-    float2 c;
+    SegConst c{sc, 0.0f};
     if (kind == kQsgd || kind == kMbit) {
-        const double sd = static_cast<double>(sc), ld = static_cast<double>(levels);
+        c.a = 0.0f;
         if (sc > 0.0f && sc <= 3.402823466e38f) {
-            c.x = static_cast<float>(ld / sd);
-            c.y = static_cast<float>(sd / ld);
-        } else {
-            c.x = 0.0f;
-            c.y = 0.0f;
+            const bool tiny = sc < 0x1.0p-64f;
+            // u * sigma is exact: a power of two times a binary32 value
+            const double sd = static_cast<double>(sc) * (tiny ? 0x1.0p64 : 1.0), lv = static_cast<double>(levels);
+            c.a = static_cast<float>(lv / sd);
+            c.b = static_cast<float>(sd / lv);
+            if (tiny) {
+                c.a = -c.a;
+                c.b = -c.b;
+            }
         }
-    } else {
-        c.x = sc;
-        c.y = 0.0f;
     }
     consts[tid] = c;
+}
+
+// r = fl(|p| s / sigma) of equation (qsgd) from the constant a of SegConst
+// (negative: |p| is first multiplied by 2^64), and the decoded magnitude
+// fl(level sigma / s) from its constant b (negative: multiplied back by
+// 2^-64).  The extra products are exact or the one final rounding.
+__device__ __forceinline__ float level_ratio(float abs_p, float ca) {
+    return mul_rn(mul_rn(abs_p, ca < 0.0f ? 0x1.0p64f : 1.0f), fabsf(ca));
+}
+__device__ __forceinline__ float level_magnitude(uint32_t level, float cb) {
+    return mul_rn(mul_rn(static_cast<float>(level), fabsf(cb)), cb < 0.0f ? 0x1.0p-64f : 1.0f);
 }
 
 // ---------------------------------------------------------------------------
@@ -168,7 +181,7 @@ struct QuadCodes {
 
 template <int KIND>
 __device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, float eta, int64_t i0, int64_t d, int m,
-                                                 const int js[4], const float2 *__restrict__ crow, int s,
+                                                 const int js[4], const SegConst *__restrict__ crow, int s,
                                                  uint32_t k0, uint32_t k1, uint32_t t) {
     QuadCodes o;
     o.sign_nib = 0u;
@@ -191,13 +204,13 @@ __device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, f
             egk = egc;
             neg = signbit(p) ? 1u : 0u;
             if (KIND == kSign) {
-                const float sc = crow[js[c]].x;
+                const float sc = crow[js[c]].a;
                 q = neg ? -sc : sc;
             } else if (KIND == kQsgd || KIND == kMbit) {
-                const float2 cs = crow[js[c]];
+                const SegConst cs = crow[js[c]];
                 const float a = fabsf(p);
-                if (cs.x > 0.0f && a > 0.0f) {
-                    const float r = mul_rn(a, cs.x);
+                if (cs.a != 0.0f && a > 0.0f) {
+                    const float r = level_ratio(a, cs.a);
                     const float l = fminf(floorf(r), fs);
                     const float frac = (l == fs) ? 0.0f : sub_rn(r, l);
                     const float u = static_cast<float>(elem(rnd, c) >> 8) * 0x1.0p-24f;
@@ -205,7 +218,7 @@ __device__ __forceinline__ QuadCodes encode_quad(const f32x4 g, const f32x4 e, f
                     lv = lv > s ? s : lv;
                     level = static_cast<uint32_t>(lv);
                 }
-                q = copysignf(mul_rn(static_cast<float>(level), cs.y), p);
+                q = copysignf(level_magnitude(level, cs.b), p);
             } else {
                 q = p;
             }
@@ -364,7 +377,7 @@ template <int KIND, int LB>
 __global__ __launch_bounds__(kBlock) void k_encode_rows(const float *__restrict__ G, float *__restrict__ E,
                                                         uint32_t *__restrict__ sign_plane,
                                                         uint32_t *__restrict__ level_plane, float *__restrict__ val,
-                                                        const float2 *__restrict__ consts,
+                                                        const SegConst *__restrict__ consts,
                                                         const int64_t *__restrict__ off,
                                                         const int32_t *__restrict__ tile_seg, RowArgs a) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
@@ -390,10 +403,10 @@ __global__ __launch_bounds__(kBlock) void k_encode_rows(const float *__restrict_
         const int m = m0 + u;
         if (m < a.M) {
             const int64_t rb = static_cast<int64_t>(m) * a.ld;
-            const float2 *crow = consts + static_cast<int64_t>(m) * a.n_seg;
+            const SegConst *crow = consts + static_cast<int64_t>(m) * a.n_seg;
             QuadCodes cq;
             if (one_seg) {
-                const float2 c1[1] = {crow[j_first]};
+                const SegConst c1[1] = {crow[j_first]};
                 cq = encode_quad<KIND>(gv[u], ev[u], a.eta, i0, a.d, m, z, c1, a.s, a.k0, a.k1, a.t);
             } else {
                 cq = encode_quad<KIND>(gv[u], ev[u], a.eta, i0, a.d, m, js, crow, a.s, a.k0, a.k1, a.t);
@@ -412,7 +425,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
                                                   float *__restrict__ W, float *__restrict__ WX,
                                                   float *__restrict__ Qhat, uint32_t *__restrict__ sign_plane,
                                                   uint32_t *__restrict__ level_plane, float *__restrict__ val,
-                                                  const float2 *__restrict__ consts, const int64_t *__restrict__ off,
+                                                  const SegConst *__restrict__ consts, const int64_t *__restrict__ off,
                                                   const int32_t *__restrict__ tile_seg, RowArgs a, float invM,
                                                   TopkArgs ta) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
@@ -504,7 +517,7 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
                                                          float *__restrict__ W, float *__restrict__ WX,
                                                          float *__restrict__ Qhat, uint32_t *__restrict__ sign_plane,
                                                          uint32_t *__restrict__ level_plane, float *__restrict__ val,
-                                                         const float2 *__restrict__ consts,
+                                                         const SegConst *__restrict__ consts,
                                                          const int64_t *__restrict__ off,
                                                          const int32_t *__restrict__ tile_seg, RowArgs a, float invM,
                                                          TopkArgs ta) {
@@ -529,14 +542,14 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
             const int64_t rb = static_cast<int64_t>(m) * a.ld;
             const f32x4 gv = ld_stream(G + rb + i0);
             const f32x4 ev = ld_stream(E + rb + i0);
-            const float2 *crow = consts + static_cast<int64_t>(m) * a.n_seg;
+            const SegConst *crow = consts + static_cast<int64_t>(m) * a.n_seg;
             QuadCodes cq;
             if constexpr (KIND == kTopk) {
                 const TopkRow *rw = ta.rows + m;
                 cq = encode_quad_topk(gv, ev, a.eta, i0, a.d, rw->T, rw->I);
             } else if (one_seg) {
-                const float2 cu = crow[j_first];
-                const float2 c4[1] = {cu};
+                const SegConst cu = crow[j_first];
+                const SegConst c4[1] = {cu};
                 const int z[4] = {0, 0, 0, 0};
                 cq = encode_quad<KIND>(gv, ev, a.eta, i0, a.d, m, z, c4, a.s, a.k0, a.k1, a.t);
             } else {
@@ -617,7 +630,7 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
 // row need it).  The magnitude is never negative, so the sign bit is set by
 // OR (-0 for a zero level with the sign bit set, as the encoder gives).
 template <int KIND, int LB, bool CHECK_D = true>
-__device__ __forceinline__ f32x4 decode_fields(uint32_t nib, uint32_t raw, const float2 *__restrict__ crow,
+__device__ __forceinline__ f32x4 decode_fields(uint32_t nib, uint32_t raw, const SegConst *__restrict__ crow,
                                                const int js[4], int64_t i0, int64_t d) {
     f32x4 out = {0.0f, 0.0f, 0.0f, 0.0f};
     uint32_t lev = 0u;
@@ -641,10 +654,10 @@ __device__ __forceinline__ f32x4 decode_fields(uint32_t nib, uint32_t raw, const
         if (CHECK_D && i0 + c >= d) continue;
         float mag;
         if (KIND == kSign) {
-            mag = crow[js[c]].x;
+            mag = crow[js[c]].a;
         } else {
             const uint32_t l = (lev >> (8 * c)) & 0xFFu;
-            mag = mul_rn(static_cast<float>(l), crow[js[c]].y);
+            mag = level_magnitude(l, crow[js[c]].b);
         }
         set_elem(out, c, __uint_as_float(__float_as_uint(mag) | (((nib >> c) & 1u) << 31)));
     }
@@ -654,7 +667,7 @@ __device__ __forceinline__ f32x4 decode_fields(uint32_t nib, uint32_t raw, const
 // Decode one quad of one row's message to p-hat.
 template <int KIND, int LB>
 __device__ __forceinline__ f32x4 decode_quad(const uint32_t *__restrict__ sign_row, const uint32_t *__restrict__ level_row,
-                                             const float *__restrict__ val_row, const float2 *__restrict__ crow,
+                                             const float *__restrict__ val_row, const SegConst *__restrict__ crow,
                                              int64_t q, int64_t d, const int js[4]) {
     const int64_t i0 = 4 * q;
     if (KIND == kIdentity) {
@@ -675,7 +688,7 @@ template <int KIND, int LB>
 __global__ __launch_bounds__(kBlock) void k_unpack(const uint32_t *__restrict__ sign_plane,
                                                    const uint32_t *__restrict__ level_plane,
                                                    const float *__restrict__ val, float *__restrict__ Phat,
-                                                   const float2 *__restrict__ consts, const int64_t *__restrict__ off,
+                                                   const SegConst *__restrict__ consts, const int64_t *__restrict__ off,
                                                    const int32_t *__restrict__ tile_seg, RowArgs a) {
     const int64_t q = static_cast<int64_t>(blockIdx.x) * kQuadsPerBlock + threadIdx.x;
     const int m = blockIdx.y;
@@ -699,7 +712,7 @@ template <int KIND, int LB>
 __global__ __launch_bounds__(kBlock) void k_aggregate(const uint32_t *__restrict__ sign_plane,
                                                       const uint32_t *__restrict__ level_plane,
                                                       const float *__restrict__ val, float *__restrict__ Qhat,
-                                                      const float2 *__restrict__ consts,
+                                                      const SegConst *__restrict__ consts,
                                                       const int64_t *__restrict__ off,
                                                       const int32_t *__restrict__ tile_seg, RowArgs a, float invM) {
     const int64_t g16 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x;  // group of 16 elements
@@ -742,7 +755,7 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(const uint32_t *__restrict
     };
     // add row m (ascending order) given its loaded fields and its constants
     auto add_row = [&](int m, uint32_t sg, const uint32_t (&fw)[kFieldWords > 0 ? kFieldWords : 1],
-                       const f32x4 (&vv)[KIND == kIdentity ? kAggQuads : 1], const float2 *crow, bool uniform) {
+                       const f32x4 (&vv)[KIND == kIdentity ? kAggQuads : 1], const SegConst *crow, bool uniform) {
 #pragma unroll
         for (int k = 0; k < kAggQuads; ++k) {
             const int64_t i0 = 4 * (q0 + k);
@@ -779,7 +792,7 @@ __global__ __launch_bounds__(kBlock) void k_aggregate(const uint32_t *__restrict
             for (int u = 0; u < kAggRows; ++u) {
                 const int m = m0 + u;
                 if (m < a.M && live) {
-                    const float2 c1[1] = {consts[static_cast<int64_t>(m) * a.n_seg + j_first]};
+                    const SegConst c1[1] = {consts[static_cast<int64_t>(m) * a.n_seg + j_first]};
                     add_row(m, sg[u], fw[u], vv[u], c1, true);
                 }
             }

@@ -25,6 +25,18 @@ constexpr int64_t kPieceElems = 32768;
 // slower.
 constexpr int64_t kPieceBlocksForLong = 16384;
 
+// Per (worker, segment) constants of the segment-scaled compressors.
+// SIGN: a = the scale.  QSGD, MBIT (equation qsgd): a = fl(s / (u sigma))
+// and b = fl(u sigma / s), where u = 2^64 for sigma < 2^-64 (so that s / sigma
+// cannot overflow binary32 and sigma / s keeps its significand) and u = 1
+// otherwise; with u = 2^64 both are stored negated, and the kernels then
+// multiply |p| by 2^64 before the product with |a| and the decoded magnitude
+// fl(level * |b|) by 2^-64.  A norm of 0 or one that is not finite gives
+// a = b = 0: level 0 everywhere.
+struct alignas(8) SegConst {
+    float a, b;
+};
+
 // Capacity of the MI355X Infinity Cache (memory-side, in front of HBM): the
 // fused pass streams message planes larger than this past the caches.
 constexpr double kInfinityCacheBytes = 256.0 * 1024 * 1024;
@@ -91,7 +103,7 @@ struct dqgan_plan_s {
     int32_t *d_seg_piece = nullptr;  // [n_seg + 1] first piece of each segment
     double *d_partial = nullptr;     // [M][n_pieces] partial sums (L1, L2^2)
     float *d_pmax = nullptr;         // [M][n_pieces] partial maxima (Linf)
-    float2 *d_consts = nullptr;      // [M][n_seg] per-segment constants
+    dq::SegConst *d_consts = nullptr;  // [M][n_seg] per-segment constants
     dq::TopkScratch topk;
 };
 

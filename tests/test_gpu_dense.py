@@ -110,10 +110,14 @@ def test_unfused_equals_fused(name):
 def test_unpack_matches_oracle_decode(name):
     """The server's decode of the message (dqgan_unpack) equals the oracle's
     decode of the same message planes."""
-    import torch
-    from oracle import oracle as orc
     w = CASES[name]()
     G, E, W = inputs(w)
+    _unpack_vs_oracle(w, G, E, W)
+
+
+def _unpack_vs_oracle(w, G, E, W):
+    import torch
+    from oracle import oracle as orc
     s = GpuState(w, G, E, W)
     s.dq.compress_ef(s.plan, w.eta, 3, s.G, s.E, None, s.wire)
     Ph = torch.full((w.M, w.ld), float("nan"), dtype=torch.float32, device=s.G.device)
@@ -276,9 +280,10 @@ def test_padding_is_never_read(name):
 @pytest.mark.parametrize("kind,extra", [("sign", {}), ("qsgd", {"levels": 15}), ("qsgd", {"levels": 255, "norm": "linf"}),
                                         ("mbit", {"levels": 8, "norm": "linf"}), ("mbit", {"levels": 4, "norm": "l2"})])
 def test_denormal_segment(kind, extra):
-    """A segment whose p is denormal (|p| ~ 1e-41, so s / sigma overflows
-    binary32 for the quantizers) next to a normal one: bit-exact against the
-    oracle, denormals kept."""
+    """A segment whose p is subnormal (|p| ~ 1e-41, so s / sigma overflows
+    binary32 for the quantizers and the 2^64-scaled evaluation of equation
+    (qsgd) applies) next to a normal one: bit-exact against the oracle,
+    subnormals kept."""
     w = custom(d=3000, M=4, kind=kind, seg_offsets=[0, 1000, 3000], eta=1.0, seed=61, group_scale=[1e-41, 1e-3],
                **extra)
     G, E, W = inputs(w, e_scale=0.0)
@@ -292,3 +297,42 @@ def test_denormal_segment(kind, extra):
     np.testing.assert_allclose(gpu["scale"], own["scale"], rtol=1e-5, atol=0)
     ref = _oracle(w, G, E, W, scales_in=gpu["scale"])
     compare_step(w, gpu, ref)
+
+
+# Segment scales across the binary32 range: subnormal p (sigma subnormal or
+# tiny), sigma just above and below s / FLT_MAX (where fl(s / sigma)
+# overflows), around 2^-64 (where the scaled evaluation starts), a normal
+# segment, and one whose 2-norm exceeds FLT_MAX with finite elements (+inf
+# scale: level 0, p-hat = +-0, e = p).
+RANGE_SCALES = [1e-41, 3e-39, 2e-38, 1e-37, 1e-30, 5e-20, 1e-3, 2e37]
+RANGE_OFFSETS = [0, 600, 1200, 1800, 2400, 3000, 3600, 4200, 5000]
+
+
+@pytest.mark.parametrize("kind,extra", [("sign", {}), ("qsgd", {"levels": 15}), ("qsgd", {"levels": 255}),
+                                        ("qsgd", {"levels": 255, "norm": "linf"}),
+                                        ("mbit", {"levels": 8, "norm": "linf"}), ("mbit", {"levels": 4, "norm": "l2"})])
+def test_norm_range_segments(kind, extra):
+    """Fused step bit-exact against the oracle (teacher-forced), the separate
+    worker and server calls equal to it, and the server's decode of the
+    message equal to the oracle's."""
+    w = custom(d=5000, M=4, kind=kind, seg_offsets=RANGE_OFFSETS, eta=1.0, seed=62, group_scale=RANGE_SCALES,
+               **extra)
+    G, E, W = inputs(w, e_scale=0.0)
+    print("case", kind, extra, flush=True)
+    a = GpuState(w, G, E, W)
+    a.fused(1)
+    gpu = a.host()
+    a.close()
+    own = _oracle(w, G, E, W)
+    np.testing.assert_allclose(gpu["scale"], own["scale"], rtol=1e-5, atol=0)
+    if w.norm == "l2":
+        assert np.all(np.isinf(gpu["scale"][:, -1]))
+    ref = _oracle(w, G, E, W, scales_in=gpu["scale"])
+    compare_step(w, gpu, ref)
+    assert np.all(np.isfinite(gpu["WX"][:, :w.d])) and np.all(np.isfinite(gpu["qhat"][:w.d]))
+    b = GpuState(w, G, E, W)
+    b.unfused(1)
+    fb = b.host()
+    b.close()
+    compare_step(w, gpu, fb)
+    _unpack_vs_oracle(w, G, E, W)
