@@ -61,7 +61,9 @@ typedef enum {
     DQGAN_EALIGN = -2,       /* a pointer is not 16-byte aligned            */
     DQGAN_ENOMEM = -3,       /* device or host allocation failed             */
     DQGAN_EHIP = -4,         /* a HIP runtime call or launch failed          */
-    DQGAN_EUNSUPPORTED = -5  /* valid, but not offered for this compressor   */
+    DQGAN_EUNSUPPORTED = -5, /* valid, but not offered for this compressor   */
+    DQGAN_ESCRATCH = -6      /* the workload exceeds the fixed scratch of
+                                dqgan_step_fused_noalloc                     */
 } dqgan_status;
 
 /* The delta-approximate compressors Q (Definition 1). */
@@ -213,6 +215,28 @@ dqgan_status dqgan_step_scales(dqgan_plan plan, float eta, const float *G, const
                                void *stream);
 dqgan_status dqgan_step_apply(dqgan_plan plan, float eta, uint32_t t, const float *G, float *E, float *W, float *WX,
                               const dqgan_wire *out, float *Qhat, void *stream);
+
+/* dqgan_step_fused without a plan and without any allocation, for callers
+ * that cannot allocate device memory: code under HIP graph capture, serving
+ * loops and harnesses that forbid hipMalloc.  Same arguments, results and
+ * buffer rules as dqgan_step_fused, with the descriptor (host; its
+ * seg_offsets are read during the call) in place of the plan.
+ *   Compressors: SIGN, QSGD, MBIT, IDENTITY; TOPK returns
+ *   DQGAN_EUNSUPPORTED.
+ *   Limit: the segment tables, the statistics pass's partial norms and the
+ *   per-segment constants live in one static 8 MiB device array per device
+ *   (held until the process ends).  They need about
+ *   12 M P + 16 P + 8 M S + ld/256 + 12 S bytes (P = number of pieces,
+ *   sum over segments of ceil(n_j / piece), piece = 32768 elements when
+ *   M * floor(d / 32768) >= 16384, else 16384; S = n_seg; every table
+ *   rounded up to 256 bytes); a workload above 8 MiB, or with more than 255
+ *   segments, returns DQGAN_ESCRATCH and enqueues nothing.
+ *   The array is shared by every call on the device and keeps the last
+ *   call's contents (every table is rewritten at each call, nothing relies
+ *   on earlier contents): calls that overlap on one device race.
+ * Enqueues kernels only (no memset, no host synchronization). */
+dqgan_status dqgan_step_fused_noalloc(const dqgan_desc *desc, float eta, uint32_t t, const float *G, float *E,
+                                      float *W, float *WX, const dqgan_wire *out, float *Qhat, void *stream);
 
 /* Static text for a status code. */
 const char *dqgan_status_string(dqgan_status status);

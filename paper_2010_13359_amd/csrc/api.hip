@@ -132,6 +132,7 @@ const char *dqgan_status_string(dqgan_status s) {
         case DQGAN_ENOMEM: return "out of memory";
         case DQGAN_EHIP: return "HIP runtime error";
         case DQGAN_EUNSUPPORTED: return "not supported for this compressor";
+        case DQGAN_ESCRATCH: return "workload exceeds the fixed scratch of dqgan_step_fused_noalloc";
     }
     return "unknown status";
 }

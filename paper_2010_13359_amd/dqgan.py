@@ -18,11 +18,11 @@ NORM_NONE, L1, L2, LINF = 0, 1, 2, 3
 KINDS = {"sign": SIGN, "qsgd": QSGD, "topk": TOPK, "identity": IDENTITY, "mbit": MBIT}
 NORMS = {"none": NORM_NONE, "l1": L1, "l2": L2, "linf": LINF}
 
-OK, EINVAL, EALIGN, ENOMEM, EHIP, EUNSUPPORTED = 0, -1, -2, -3, -4, -5
+OK, EINVAL, EALIGN, ENOMEM, EHIP, EUNSUPPORTED, ESCRATCH = 0, -1, -2, -3, -4, -5, -6
 
 EXPORTS = ("dqgan_plan_create", "dqgan_plan_destroy", "dqgan_wire_bytes", "dqgan_compress_ef", "dqgan_pack",
            "dqgan_unpack", "dqgan_aggregate", "dqgan_omd_step", "dqgan_step_fused", "dqgan_step_scales",
-           "dqgan_step_apply", "dqgan_status_string")
+           "dqgan_step_apply", "dqgan_step_fused_noalloc", "dqgan_status_string")
 
 
 class DqganError(RuntimeError):
@@ -70,6 +70,8 @@ def load():
     L.dqgan_step_fused.argtypes = [P, f32, u32, P, P, P, P, ctypes.POINTER(WireStruct), P, P]
     L.dqgan_step_scales.argtypes = [P, f32, P, P, ctypes.POINTER(WireStruct), P]
     L.dqgan_step_apply.argtypes = [P, f32, u32, P, P, P, P, ctypes.POINTER(WireStruct), P, P]
+    L.dqgan_step_fused_noalloc.argtypes = [ctypes.POINTER(Desc), f32, u32, P, P, P, P, ctypes.POINTER(WireStruct),
+                                           P, P]
     L.dqgan_status_string.argtypes = [i32]
     L.dqgan_status_string.restype = ctypes.c_char_p
     for name in EXPORTS:
@@ -250,3 +252,14 @@ def step_apply(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
     _check("dqgan_step_apply", load().dqgan_step_apply(plan.handle, ctypes.c_float(eta), t, plan._mat(G, "G"),
                                                        plan._mat(E, "E"), plan._vec(W, "W"), plan._mat(WX, "WX"),
                                                        ctypes.byref(ws), plan._vec(Qhat, "Qhat"), _stream(stream)))
+
+
+def step_fused_noalloc(plan, eta, t, G, E, W, WX, wire, Qhat=None, stream=None):
+    """dqgan_step_fused_noalloc with the descriptor of `plan` (the plan only
+    supplies the descriptor and the byte sizes the arguments are checked
+    against; the call itself uses neither the plan nor any allocation)."""
+    ws = wire.struct(plan)
+    _check("dqgan_step_fused_noalloc",
+           load().dqgan_step_fused_noalloc(ctypes.byref(plan.desc), ctypes.c_float(eta), t, plan._mat(G, "G"),
+                                           plan._mat(E, "E"), plan._vec(W, "W"), plan._mat(WX, "WX"),
+                                           ctypes.byref(ws), plan._vec(Qhat, "Qhat"), _stream(stream)))
