@@ -1,18 +1,17 @@
 """GPU parity at the benchmark's full sizes, in the launch configuration
 bench.py times (dqgan_step_scales then dqgan_step_apply), on the gradient
-batches bench.py draws.
+batches bench.py draws: one teacher-forced iteration.
 
 C2 (d = 6.3M, M = 16, s = 255) and C5 (the same shape, 8-bit Appendix A
 codes, infinity norm): every output against the oracle.
-C3 (d = 33.5M, M = 32, s = 15): sampled segments (the smallest, a middle one,
-the largest), all workers, element by element against the oracle.
-C2 and C5 also free-running over three iterations (each side on its own
-state, its own scales), every output against the oracle; C3 and C6
-free-running on the sampled segments.
 C4 (d = 1e8, M = 64, top-k k = 1e6): sampled workers checked for the exact
 top-k property (ties to the lower index) from their p, residuals exact, and
 the server average / OMD outputs on sampled column windows against the
-oracle, fed the messages of all workers."""
+oracle, fed the messages of all workers.
+
+The whole trajectories of every workload (C3 and C6 teacher-forced over
+every segment, C4 over every row and iteration) are in
+test_gpu_trajectories.py."""
 import numpy as np
 import pytest
 
@@ -82,56 +81,6 @@ def test_c2_c5_full_teacher_forced(index):
 
 
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("index", [3, 6])
-def test_c3_c6_sampled_segments(index):
-    """C3: 4-bit quantizer, L2; C6: the same shape with the paper's 8-bit
-    sign-magnitude codes and the infinity-norm scale."""
-    from oracle import oracle as orc
-    import synth
-    w = synth.get(index)
-    print("C%d sampled" % index, flush=True)
-    plan, G, pre, E, W, WX, wire = _run(w)
-    t = 2
-    sizes = np.diff(w.seg_offsets)
-    picks = sorted({int(np.argmin(sizes)), int(np.argsort(sizes)[len(sizes) // 2]), int(np.argmax(sizes))})
-    scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
-    mbit = w.kind == "mbit"
-    k_levels = (1 << (w.levels - 1)) - 1 if mbit else w.levels
-    sign_rows = None if mbit else wire.sign.view(w.M, -1).cpu().numpy().view(np.uint32)
-    level_rows = wire.level.view(w.M, -1).cpu().numpy().view(np.uint32)
-    eta = np.float32(w.eta)
-    for j in picks:
-        a, b = w.seg_offsets[j], w.seg_offsets[j + 1]
-        n = b - a
-        Gs = G[:, a:b].cpu().numpy()
-        Es = pre["E"][:, a:b].cpu().numpy()
-        Ws = pre["W"][a:b].cpu().numpy()
-        phat = np.empty((w.M, n), np.float32)
-        enew = np.empty((w.M, n), np.float32)
-        for m in range(w.M):
-            p = orc.ef_accumulate(eta, Gs[m], Es[m])
-            own = orc.scale(p, w.norm)
-            assert abs(float(scales[m, j]) - float(own)) <= 1e-5 * float(own), (j, m)
-            bits, lv, ph, e = orc.qsgd_encode(p, scales[m, j], k_levels, w.quant_seed, m, t, i0=a)
-            phat[m], enew[m] = ph, e
-            if mbit:
-                codes = orc.unpack_bits(level_rows[m], w.levels, b)[a:b]
-                assert_same("codes seg %d row %d" % (j, m), codes, orc.mbit_fields(bits, lv, w.levels))
-            else:
-                gs = orc.unpack_bits(sign_rows[m], 1, b)[a:b]
-                gl = orc.unpack_bits(level_rows[m], 4, b)[a:b]
-                assert_same("sign bits seg %d row %d" % (j, m), gs, bits.astype(np.uint16))
-                assert_same("levels seg %d row %d" % (j, m), gl, lv)
-        assert_same("e_t seg %d" % j, E[:, a:b].cpu().numpy(), enew)
-        q = orc.aggregate(phat, n)
-        wt = orc.omd_update(q, Ws)
-        assert_same("w_t seg %d" % j, W[a:b].cpu().numpy(), wt)
-        wx = np.stack([orc.extrapolate(eta, wt, Gs[m], enew[m]) for m in range(w.M)])
-        assert_same("WX seg %d" % j, WX[:, a:b].cpu().numpy(), wx)
-    plan.close()
-
-
-@pytest.mark.timeout(300)
 def test_c4_sampled_rows_and_windows():
     from oracle import oracle as orc
     import synth
@@ -177,139 +126,3 @@ def test_c4_sampled_rows_and_windows():
         wx = np.stack([orc.extrapolate(eta, wt, Gs[m], Es[m]) for m in range(w.M)])
         assert_same("WX window %d" % a, WX[:, a:b].cpu().numpy(), wx)
     plan.close()
-
-
-@pytest.mark.timeout(600)
-@pytest.mark.parametrize("index", [2, 5])
-def test_c2_c5_free_running(index):
-    """Three iterations at full size on each side's own state (gradients are
-    inputs, as in the benchmark).  Each side computes its own scales; they
-    agree within 1e-5 (binary64 sums in different orders, rounded once), so
-    a level can differ only at a near-tie of the rounding: such elements are
-    counted (at most 1 in 10^6 per step) and must differ by exactly one level
-    step in e_t; every other element of e_t, w_t and WX within 1e-5 relative
-    of the operand magnitude of its last operation."""
-    import torch
-    import synth
-    from oracle import oracle as orc
-    from paper_2010_13359_amd import dqgan
-    from gpu_common import rel_close, to_dev
-    w = synth.get(index)
-    print("C%d free-running" % index, flush=True)
-    d = w.d
-    E_r = np.zeros((w.M, w.ld), np.float32)
-    W_r = synth.init_params_np(w)
-    plan = dqgan.Plan.from_workload(w)
-    dev = torch.device("cuda:0")
-    E, W = to_dev(E_r), to_dev(W_r)
-    WX = torch.empty((w.M, w.ld), dtype=torch.float32, device=dev)
-    wire = plan.new_wire(dev)
-    eta = np.float32(w.eta)
-    k_levels = (1 << (w.levels - 1)) - 1 if w.kind == "mbit" else w.levels
-    ties = 0
-    for t in range(1, 4):
-        G = synth.gradients_np(w, t)
-        dqgan.step_fused(plan, w.eta, t, to_dev(G), E, W, WX, wire)
-        torch.cuda.synchronize()
-        P = np.abs(eta * G[:, :d]) + np.abs(E_r[:, :d])
-        W_prev = W_r[:d].copy()
-        ref = orc.step(w.as_dict(), eta, t, G, E_r, W_r)
-        gE, gW, gWX = E.cpu().numpy(), W.cpu().numpy(), WX.cpu().numpy()
-        scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
-        rel_close("scale", scales, ref["scale"], tau=1e-30)
-        bad = gE[:, :d] != ref["E"][:, :d]
-        n_bad = int(bad.sum())
-        assert n_bad <= 1e-6 * w.M * d, (t, n_bad)
-        if n_bad:
-            rows, cols = np.nonzero(bad)
-            seg = np.searchsorted(w.seg_offsets, cols, side="right") - 1
-            step = ref["scale"][rows, seg].astype(np.float64) / k_levels
-            diff = np.abs(gE[rows, cols].astype(np.float64) - ref["E"][rows, cols].astype(np.float64))
-            assert np.all(np.abs(diff - step) <= 1e-5 * step + 1e-30), (t, diff[:5], step[:5])
-        ties += n_bad
-        keep = ~bad
-        rel_close("E", np.where(keep, gE[:, :d], ref["E"][:, :d]), ref["E"][:, :d], tau=P + 1e-30)
-        X = np.abs(eta * G[:, :d]) + np.abs(E_r[:, :d])
-        # columns holding a near-tie carry its one-step difference into q-hat, w_t and WX
-        cols_ok = ~bad.any(axis=0)
-        rel_close("W", gW[:d][cols_ok], ref["W"][:d][cols_ok],
-                  tau=(np.abs(W_prev) + np.abs(ref["qhat"][:d]) + 1e-30)[cols_ok])
-        rel_close("WX", gWX[:, :d][:, cols_ok], ref["WX"][:, :d][:, cols_ok],
-                  tau=(np.abs(W_r[None, :d]) + X + 1e-30)[:, cols_ok])
-    plan.close()
-    print("near-tie level differences over 3 steps: %d" % ties)
-
-
-@pytest.mark.timeout(600)
-@pytest.mark.parametrize("index", [3, 6])
-def test_c3_c6_free_running_sampled_segments(index):
-    """Three iterations at full size in the launch configuration bench.py
-    times, each side on its own state.  Every quantity of the iteration is a
-    function of the columns of whole segments (scales per segment, the
-    average, update and evaluation point per column), so the oracle follows
-    the sampled segments (the smallest, a middle one, the largest) of all
-    workers on their own, with the global element index for the generator
-    counter.  Checks as in the C2/C5 free run: scales within 1e-5; e_t exact
-    except for counted near-ties of the rounding (one level step apart);
-    w_t and WX within 1e-5 relative of their last operation's operands."""
-    import torch
-    import synth
-    from oracle import oracle as orc
-    from paper_2010_13359_amd import dqgan
-    from gpu_common import rel_close
-    w = synth.get(index)
-    print("C%d free-running, sampled segments" % index, flush=True)
-    sizes = np.diff(w.seg_offsets)
-    picks = sorted({int(np.argmin(sizes)), int(np.argsort(sizes)[len(sizes) // 2]), int(np.argmax(sizes))})
-    dev = torch.device("cuda:0")
-    plan = dqgan.Plan.from_workload(w)
-    E = torch.zeros((w.M, w.ld), dtype=torch.float32, device=dev)
-    W = synth.init_params(w, device=dev)
-    WX = torch.empty((w.M, w.ld), dtype=torch.float32, device=dev)
-    wire = plan.new_wire(dev)
-    eta = np.float32(w.eta)
-    k_levels = (1 << (w.levels - 1)) - 1 if w.kind == "mbit" else w.levels
-    seg = {j: (w.seg_offsets[j], w.seg_offsets[j + 1]) for j in picks}
-    E_r = {j: np.zeros((w.M, b - a), np.float32) for j, (a, b) in seg.items()}
-    W_r = {j: W[a:b].cpu().numpy() for j, (a, b) in seg.items()}
-    G = None
-    ties = 0
-    for t in range(1, 4):
-        G = synth.gradients(w, t, device=dev, out=G)
-        dqgan.step_scales(plan, w.eta, G, E, wire)
-        dqgan.step_apply(plan, w.eta, t, G, E, W, WX, wire)
-        torch.cuda.synchronize()
-        scales = wire.scale.view(w.M, w.n_seg).cpu().numpy()
-        for j, (a, b) in seg.items():
-            n = b - a
-            Gs = G[:, a:b].cpu().numpy()
-            own = np.empty(w.M, np.float32)
-            phat = np.empty((w.M, n), np.float32)
-            enew = np.empty((w.M, n), np.float32)
-            for m in range(w.M):
-                p = orc.ef_accumulate(eta, Gs[m], E_r[j][m])
-                own[m] = orc.scale(p, w.norm)
-                _, _, phat[m], enew[m] = orc.qsgd_encode(p, own[m], k_levels, w.quant_seed, m, t, i0=a)
-            rel_close("scale seg %d step %d" % (j, t), scales[:, j], own, tau=1e-30)
-            wt = orc.omd_update(orc.aggregate(phat, n), W_r[j])
-            wx = np.stack([orc.extrapolate(eta, wt, Gs[m], enew[m]) for m in range(w.M)])
-            gE, gW, gWX = E[:, a:b].cpu().numpy(), W[a:b].cpu().numpy(), WX[:, a:b].cpu().numpy()
-            bad = gE != enew
-            n_bad = int(bad.sum())
-            assert n_bad <= max(1, 1e-6 * w.M * n), (j, t, n_bad)
-            if n_bad:
-                rows, _ = np.nonzero(bad)
-                step = own[rows].astype(np.float64) / k_levels
-                diff = np.abs(gE[bad].astype(np.float64) - enew[bad].astype(np.float64))
-                assert np.all(np.abs(diff - step) <= 1e-5 * step + 1e-30), (j, t, diff[:5], step[:5])
-            ties += n_bad
-            X = np.abs(eta * Gs) + np.abs(enew)
-            cols_ok = ~bad.any(axis=0)
-            rel_close("W seg %d step %d" % (j, t), gW[cols_ok], wt[cols_ok],
-                      tau=(np.abs(W_r[j]) + np.abs(wt - W_r[j]) + 1e-30)[cols_ok])
-            rel_close("WX seg %d step %d" % (j, t), gWX[:, cols_ok], wx[:, cols_ok],
-                      tau=(np.abs(wt[None, :]) + X + 1e-30)[:, cols_ok])
-            E_r[j], W_r[j] = enew, wt
-        print("step %d done" % t, flush=True)
-    plan.close()
-    print("near-tie level differences over 3 steps: %d" % ties)
