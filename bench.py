@@ -7,14 +7,17 @@ as the two passes of the library (dqgan_step_scales, dqgan_step_apply).
 Inputs (gradients, residuals, parameters) are resident in HBM before the timed
 region; two gradient batches alternate between steps.
 
-Prints one JSON line.  `value` is gradient GB/s = M * d * 4 bytes / step time.
+Prints one JSON line.  `value` is gradient GB/s = M * d * 4 bytes / step time
+of the headline workload (C3 unless --config says otherwise); by default
+`also_measured` carries the same record for C4 (top-k, 64 x 10^8), timed
+in the same process after it.
 `roofline` is the dominant kernel (the apply pass) against the 8 TB/s HBM
 peak, with its algorithmic bytes per launch; `step_roofline` is the same for
 the whole step, plus the HBM bytes the rocprofv3 counters measured for the
 step's two main kernels (profiles/traffic.json) over the step time.  `cpu_baseline` is the oracle (single-threaded C) on a
 bounded sample of the same workload.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--graph]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 3] [--also 4|none] [--graph]
 """
 import argparse
 import hashlib
@@ -171,31 +174,16 @@ def cpu_baseline(w, target_elems=4_000_000):
                                                                                  os.cpu_count() or 0)}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=3, help="workload index C0..C6 (default C3)")
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run a plain device copy of 1 GiB (counter calibration)")
-    ap.add_argument("--graph", action="store_true",
-                    help="capture the timed iterations in one HIP graph and time its replay (launch-bound sizes); "
-                         "the per-pass times then come from an eager run of the same iterations")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py: the library runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
-              "one batched matrix on a single device)" % args.gpus, file=sys.stderr)
-        sys.exit(2)
-
+def measure(w, steps, warmup, graph_mode=False, copy_calibration=False, extras=True):
+    """Time `steps` iterations of workload `w` (after `warmup` untimed ones)
+    on cuda:0 and return the record: step time, gradient GB/s, the apply
+    pass against the HBM peak (`roofline`), the whole step (`step_roofline`)
+    and, with `extras`, the reference streams and the separate calls."""
     import torch
     import synth
     from paper_2010_13359_amd import dqgan
 
-    w = synth.get(args.config)
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
     print("bench: workload %s" % workload_label(w), file=sys.stderr, flush=True)
     plan = dqgan.Plan.from_workload(w)
     Gs = [synth.gradients(w, t, device=dev) for t in (1, 2)]
@@ -216,44 +204,44 @@ def main():
         if ev:
             ev[2].record()
 
-    for t in range(1, args.warmup + 1):
+    for t in range(1, warmup + 1):
         one(t)
     torch.cuda.synchronize()
-    if args.copy_calibration:
+    if copy_calibration:
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
         for _ in range(3):
             b.copy_(a)
         torch.cuda.synchronize()
         del a, b
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     graph = None
-    if args.graph:
+    if graph_mode:
         graph = torch.cuda.CUDAGraph()
         with torch.cuda.graph(graph):
-            for k in range(args.steps):
-                one(args.warmup + 1 + k)
+            for k in range(steps):
+                one(warmup + 1 + k)
     torch.cuda.synchronize()
     t_wall = time.perf_counter()
     start.record()
     if graph is not None:
         graph.replay()
     else:
-        for k in range(args.steps):
-            one(args.warmup + 1 + k, evs[k])
+        for k in range(steps):
+            one(warmup + 1 + k, evs[k])
     stop.record()
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     total_ms = start.elapsed_time(stop)
     if graph is not None:
         # per-pass times: the same iterations again, eagerly, with events
-        for k in range(args.steps):
-            one(args.warmup + 1 + k, evs[k])
+        for k in range(steps):
+            one(warmup + 1 + k, evs[k])
         torch.cuda.synchronize()
     scales_ms = [e[0].elapsed_time(e[1]) for e in evs]
     apply_ms = [e[1].elapsed_time(e[2]) for e in evs]
-    ms_step = total_ms / args.steps
+    ms_step = total_ms / steps
     grad_bytes = w.M * w.d * 4.0
     value = grad_bytes / (ms_step * 1e-3) / 1e9
     b_alg = algorithmic_bytes(w)
@@ -267,12 +255,11 @@ def main():
     stats_traffic = traffic_record("stats_C%d" % w.index, "topk" if w.kind == "topk" else "dense")
     step_counter = (traffic + stats_traffic) if (traffic and stats_traffic) else None
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "value": round(value, 2), "unit": "GB/s", "steps": steps, "warmup": warmup,
+        "ms_per_step": round(ms_step, 4),
         "config": {"workload": workload_label(w), "d": w.d, "M": w.M, "compressor": w.kind, "levels": w.levels,
                    "k": w.k, "segments": w.n_seg, "parallelism": "single GPU; M workers as rows",
-                   "launch": "hip graph of the timed iterations" if args.graph else "eager"},
+                   "launch": "hip graph of the timed iterations" if graph_mode else "eager"},
         "roofline": {"bound": "hbm", "kernel": "dqgan_step_apply (fused encode+EF+aggregate+OMD pass)",
                      "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
@@ -323,11 +310,54 @@ def main():
                            "step_frac_of_copy": round(step_ach / cp_gbs, 4),
                            "step_counter_frac_of_copy": (round(step_counter / (ms_step * 1e-3) / 1e9 / cp_gbs, 4)
                                                          if step_counter else None)}
-    out["separate_calls"] = separate_calls(plan, w, Gs[0], E, W, WX, wire, dev)
+    if extras:
+        out["separate_calls"] = separate_calls(plan, w, Gs[0], E, W, WX, wire, dev)
     del graph
     plan.close()
     del Gs, E, W, WX, wire
     torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=3, help="workload index C0..C6 (default C3)")
+    ap.add_argument("--also", default=None,
+                    help="comma-separated workload indices timed after the headline one and reported in "
+                         "`also_measured` (default: 4 when the headline is C3, else none; 'none' for none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a plain device copy of 1 GiB (counter calibration)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the timed iterations in one HIP graph and time its replay (launch-bound sizes); "
+                         "the per-pass times then come from an eager run of the same iterations")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: the library runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
+              "one batched matrix on a single device)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import synth
+
+    torch.cuda.set_device(torch.device("cuda:0"))
+    w = synth.get(args.config)
+    rec = measure(w, args.steps, args.warmup, args.graph, args.copy_calibration)
+    out = {"metric": METRIC, "value": rec.pop("value"), "unit": rec.pop("unit"), "n_gpus": 1,
+           "steps": rec.pop("steps"), "warmup": rec.pop("warmup"), "ms_per_step": rec.pop("ms_per_step"),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic"}
+    out.update(rec)
+    also = args.also if args.also is not None else ("4" if args.config == 3 else "none")
+    if also != "none":
+        # the other workload the HBM target names (C4, top-k over 64 x 10^8),
+        # timed in the same process after the headline one
+        out["also_measured"] = []
+        for idx in [int(x) for x in also.split(",") if x.strip()]:
+            other = measure(synth.get(idx), args.steps, min(args.warmup, 3), args.graph, extras=False)
+            out["also_measured"].append(other)
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on a sample", file=sys.stderr, flush=True)
         # about 10-30 s of single-core work: the sort-based top-k oracle is

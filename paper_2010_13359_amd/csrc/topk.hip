@@ -242,132 +242,142 @@ __global__ __launch_bounds__(1024) void k_topk_band(const uint32_t *__restrict__
 }
 
 // 3. Full pass: per tile the count of keys above the band, and the in-band
-// candidates appended to the row's list.  A workgroup covers 64 tiles of one
-// row in four rounds (each: 4 waves x 4 tiles, loaded before any is examined)
-// and appends its candidates with one atomic; four rounds per workgroup
-// rather than one spread its fixed costs (row bounds, staging set-up, the
-// final atomic) over 16384 elements.  A tile wholly below d (all but the
-// last of a row) is classified without per-element bounds tests, on masks
-// taken straight from the comparisons: half the vector instructions of the
-// bounds-tested form, which made the pass 2 % slower.
+// candidates appended to the row's list.  A workgroup covers 64 consecutive
+// tiles of one row; wave w owns 16 consecutive tiles of them, four per round
+// (the round's eight loads issued before its first tile is examined).  Lane j
+// of a wave keeps the count of the wave's j-th tile, and the wave writes its
+// 16 counts with one 64-byte store at the end: over 64 rows of 10^8 elements
+// a 4-byte count store per tile held the pass 8 % above its loads alone.
+// Candidates are staged in the wave's quarter of an LDS buffer with a
+// wave-uniform count (a wave whose quarter overflows appends straight to the
+// row's list); at the end the workgroup adds its above-band total and its
+// staged candidates to the row with one atomic each.  A tile wholly below d
+// (all but the last of a row) is classified without per-element bounds
+// tests, on masks taken straight from the comparisons.
 constexpr int kPassRounds = 4;
+constexpr int kPassTilesPerWave = 4 * kPassRounds;
+constexpr int kPassTilesPerBlock = kPassTilesPerWave * (kBlock / 64);
 __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                       TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
                                                       uint2 *__restrict__ cand, int64_t cap) {
-    // Candidates are staged in a small LDS buffer (few per tile are in the
-    // band); a wave whose reservation does not fit appends straight to the
-    // row's list, and only the valid prefix [0, valid_end) is flushed.
-    constexpr uint32_t kStage = 1024;
-    __shared__ uint2 buf[kStage];
-    __shared__ uint32_t nbuf, base, nab, valid_end;
+    constexpr uint32_t kStage = 256;  // staged candidates per wave
+    constexpr int kWaves = kBlock / 64;
+    __shared__ uint2 buf[kWaves][kStage];
+    __shared__ uint32_t wave_nab[kWaves], wave_ns[kWaves], base;
     const int m = blockIdx.y;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint32_t lo = rows[m].lo, hi = rows[m].hi;
     const float *g = G + static_cast<int64_t>(m) * ld;
     const float *e = E + static_cast<int64_t>(m) * ld;
-    if (threadIdx.x == 0) {
-        nbuf = 0;
-        nab = 0;
-        valid_end = kStage;
-    }
-    __syncthreads();
     const uint32_t span = hi - lo;
     uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    uint2 *stage = buf[wave];
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kPassTilesPerBlock + kPassTilesPerWave * wave;
+    uint32_t my_cnt = 0;  // lane j < 16: above-band count of tile t0 + j
+    uint32_t nab = 0;     // wave-uniform: keys above the band in the wave's tiles
+    uint32_t ns = 0;      // wave-uniform: candidates staged by the wave
     for (int round = 0; round < kPassRounds; ++round) {
-        const int64_t tb = (static_cast<int64_t>(blockIdx.x) * kPassRounds + round) * 16;
-        // The wave's four tiles of this round are loaded before any is examined.
+        // Unconditional loads (a tile past the row's end reads the last tile
+        // again and is not examined): loads under a branch made the compiler
+        // wait for each tile's loads before issuing the next tile's.
         f32x4 gvs[4], evs[4];
 #pragma unroll
         for (int it = 0; it < 4; ++it) {
-            const int64_t tile = tb + it * 4 + wave;
-            if (tile < n_tiles) {
-                const int64_t i0 = tile * kTopkTile + 4 * lane;
-                gvs[it] = ld_stream(g + i0);
-                evs[it] = ld_stream(e + i0);
-            }
+            const int64_t tile = t0 + 4 * round + it;
+            const int64_t i0 = (tile < n_tiles ? tile : n_tiles - 1) * kTopkTile + 4 * lane;
+            gvs[it] = ld_stream(g + i0);
+            evs[it] = ld_stream(e + i0);
         }
 #pragma unroll
         for (int it = 0; it < 4; ++it) {
-            const int64_t tile = tb + it * 4 + wave;
-            if (tile < n_tiles) {
-                const int64_t i0 = tile * kTopkTile + 4 * lane;
-                // Only the last tile of a row can hold elements at or beyond d.
-                const bool full = (tile + 1) * kTopkTile <= d;
-                uint32_t keys[4];
-                uint64_t cb[4];  // wave masks of the in-band candidates, per element of the quad
-                uint32_t above_n = 0, tot = 0;
+            // A tile past the row's end (only in a row's last workgroup) is
+            // examined too, with no element valid; the loads stay ahead of
+            // every tile's work only if no tile's work is conditional.
+            const int64_t tile = t0 + 4 * round + it;
+            const int64_t i0 = tile * kTopkTile + 4 * lane;
+            const int64_t end = tile < n_tiles ? d : 0;  // elements [0, end) of the row are valid here
+            // Only the last tile of a row can hold elements at or beyond d.
+            const bool full = (tile + 1) * kTopkTile <= end;
+            uint32_t keys[4];
+            uint64_t cb[4];  // wave masks of the in-band candidates, per element of the quad
+            uint32_t above_n = 0, tot = 0;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) keys[k] = key_of(elem(gvs[it], k), elem(evs[it], k), eta);
-                if (full) {
+            for (int k = 0; k < 4; ++k) keys[k] = key_of(elem(gvs[it], k), elem(evs[it], k), eta);
+            if (full) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    above_n += __popcll(__builtin_amdgcn_ballot_w64(keys[k] > hi));
+                    cb[k] = __builtin_amdgcn_ballot_w64(keys[k] - lo <= span);  // lo <= key <= hi
+                    tot += __popcll(cb[k]);
+                }
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const bool valid = i0 + k < end;
+                    above_n += __popcll(__builtin_amdgcn_ballot_w64(valid && keys[k] > hi));
+                    cb[k] = __builtin_amdgcn_ballot_w64(valid && keys[k] - lo <= span);
+                    tot += __popcll(cb[k]);
+                }
+            }
+            my_cnt = lane == 4 * round + it ? above_n : my_cnt;
+            nab += above_n;
+            if (tot) {
+                // this lane's first slot: the wave's candidates in lower lanes
+                uint32_t pre = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    pre = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(cb[k] >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(cb[k]), pre));
+                if (ns + tot <= kStage) {
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        above_n += __popcll(__builtin_amdgcn_ballot_w64(keys[k] > hi));
-                        cb[k] = __builtin_amdgcn_ballot_w64(keys[k] - lo <= span);  // lo <= key <= hi
-                        tot += __popcll(cb[k]);
+                        if ((cb[k] >> lane) & 1u) {
+                            stage[ns + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                            ++pre;
+                        }
                     }
+                    ns += tot;
                 } else {
+                    uint32_t gbase = 0;
+                    if (lane == 0) gbase = atomicAdd(&rows[m].n_cand, tot);
+                    gbase = __builtin_amdgcn_readfirstlane(gbase);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        const bool valid = i0 + k < d;
-                        above_n += __popcll(__builtin_amdgcn_ballot_w64(valid && keys[k] > hi));
-                        cb[k] = __builtin_amdgcn_ballot_w64(valid && keys[k] - lo <= span);
-                        tot += __popcll(cb[k]);
-                    }
-                }
-                if (lane == 0) {
-                    tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = above_n;
-                    if (above_n) atomicAdd(&nab, above_n);
-                }
-                if (tot) {
-                    // this lane's first slot: the wave's candidates in lower lanes
-                    uint32_t pre = 0;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k)
-                        pre = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(cb[k] >> 32),
-                                                        __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(cb[k]), pre));
-                    uint32_t wbase = 0;
-                    if (lane == 0) wbase = atomicAdd(&nbuf, tot);
-                    wbase = __builtin_amdgcn_readfirstlane(wbase);
-                    if (wbase + tot <= kStage) {
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) {
-                            if ((cb[k] >> lane) & 1u) {
-                                buf[wbase + pre] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
-                                ++pre;
-                            }
-                        }
-                    } else {
-                        uint32_t gbase = 0;
-                        if (lane == 0) {
-                            atomicMin(&valid_end, wbase);
-                            gbase = atomicAdd(&rows[m].n_cand, tot);
-                        }
-                        gbase = __builtin_amdgcn_readfirstlane(gbase);
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) {
-                            if ((cb[k] >> lane) & 1u) {
-                                const int64_t pos = static_cast<int64_t>(gbase) + pre;
-                                if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
-                                ++pre;
-                            }
+                        if ((cb[k] >> lane) & 1u) {
+                            const int64_t pos = static_cast<int64_t>(gbase) + pre;
+                            if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                            ++pre;
                         }
                     }
                 }
             }
         }
     }
-    __syncthreads();
-    const uint32_t n_valid = nbuf < valid_end ? nbuf : valid_end;
-    if (threadIdx.x == 0) {
-        base = n_valid ? atomicAdd(&rows[m].n_cand, n_valid) : 0u;
-        if (nab) atomicAdd(&rows[m].n_above, nab);
+    // the wave's 16 tile counts: lanes 0..15, one contiguous store
+    if (lane < kPassTilesPerWave && t0 + lane < n_tiles) tile_cnt[static_cast<int64_t>(m) * n_tiles + t0 + lane] = my_cnt;
+    if (lane == 0) {
+        wave_nab[wave] = nab;
+        wave_ns[wave] = ns;
     }
     __syncthreads();
-    for (uint32_t j = threadIdx.x; j < n_valid; j += kBlock) {
-        const int64_t pos = static_cast<int64_t>(base) + j;
-        if (pos < cap) crow[pos] = buf[j];
+    if (threadIdx.x == 0) {
+        uint32_t a = 0, n = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            a += wave_nab[w];
+            n += wave_ns[w];
+        }
+        if (a) atomicAdd(&rows[m].n_above, a);
+        base = n ? atomicAdd(&rows[m].n_cand, n) : 0u;
+    }
+    __syncthreads();
+    uint32_t off = base;
+    for (int w = 0; w < wave; ++w) off += wave_ns[w];
+    for (uint32_t j = lane; j < ns; j += 64) {
+        const int64_t pos = static_cast<int64_t>(off) + j;
+        if (pos < cap) crow[pos] = stage[j];
     }
 }
 
@@ -905,7 +915,7 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kSampleThreads), 0, st,
                        G, E, eta, D.d, D.ld, S.n_chunks, S.hist);
     hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
-    const int64_t per_block = 16 * kPassRounds;
+    const int64_t per_block = kPassTilesPerBlock;
     hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + per_block - 1) / per_block), M),
                        dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
     hipLaunchKernelGGL(k_topk_select, dim3(M), dim3(1024), 0, st, S.rows, S.cand, S.cap, D.k, S.hist);
