@@ -166,15 +166,17 @@ dqgan_status dqgan_wire_bytes(dqgan_plan plan, size_t *sign, size_t *level, size
 dqgan_status dqgan_compress_ef(dqgan_plan plan, float eta, uint32_t t, const float *G, float *E,
                                const float *scales_in, const dqgan_wire *out, void *stream);
 
-/* Pack per-element codes into the message planes (SIGN, QSGD, MBIT).
+/* Pack per-element codes into the message planes (SIGN, QSGD, MBIT): the
+ * worker's push of p-hat to the server in Algorithm 2, for codes the caller
+ * computed itself.
  *   codes: [M][ld] uint16; bit 15 = sign bit, bits 0..14 = level (QSGD, MBIT;
  *   must be <= s, resp. k).  scales: [M][n_seg], copied to out->scale.
  * TOPK and IDENTITY return DQGAN_EUNSUPPORTED. */
 dqgan_status dqgan_pack(dqgan_plan plan, const uint16_t *codes, const float *scales, const dqgan_wire *out,
                         void *stream);
 
-/* Decode the M messages to the dense p-hat [M][ld] (what the server sees
- * after pulling them).  SIGN: +-scale; QSGD: copysign(fl(level * fl(sigma/s)),
+/* Decode the M messages to the dense p-hat [M][ld]: what the server holds
+ * after pulling the workers' pushed messages in Algorithm 2.  SIGN: +-scale; QSGD: copysign(fl(level * fl(sigma/s)),
  * sign); MBIT: the same with s = k; TOPK: val at idx, 0 elsewhere; IDENTITY:
  * val. */
 dqgan_status dqgan_unpack(dqgan_plan plan, const dqgan_wire *in, float *Phat, void *stream);
@@ -192,7 +194,9 @@ dqgan_status dqgan_aggregate(dqgan_plan plan, const dqgan_wire *in, float *Qhat,
 dqgan_status dqgan_omd_step(dqgan_plan plan, float eta, const float *Qhat, float *W, const float *G,
                             const float *E, float *WX, void *stream);
 
-/* The whole iteration in as few passes over HBM as the data dependences
+/* One whole iteration of Algorithm 2 (every worker step, the push of the
+ * messages, the server's pull and average, the update and the next
+ * evaluation points) in as few passes over HBM as the data dependences
  * allow: dqgan_compress_ef, then the server average of the M messages
  * (decoded in registers, not re-read from the message), dqgan_omd_step.
  * Results equal those of the separate calls bit for bit.

@@ -19,6 +19,9 @@ _DIR = os.environ.get("DQGAN_ORACLE_DIR") or _HERE
 SRC = os.path.join(_DIR, "dqgan_oracle.c")
 LIB = os.path.join(_DIR, "libdqgan_oracle.so")
 CFLAGS = ["-O2", "-std=c11", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared"]
+# DQGAN_ORACLE_EXTRA_CFLAGS adds flags (the sanitizer test builds an
+# instrumented copy with it).
+EXTRA_CFLAGS = os.environ.get("DQGAN_ORACLE_EXTRA_CFLAGS", "").split()
 
 KIND = {"sign": 0, "qsgd": 1, "topk": 2, "identity": 3, "mbit": 4}
 NORM = {"l1": 1, "l2": 2, "linf": 3}
@@ -27,7 +30,7 @@ NORM = {"l1": 1, "l2": 2, "linf": 3}
 def build():
     """Compile the oracle with gcc (no FMA contraction, no fast-math)."""
     tmp = LIB + ".tmp%d" % os.getpid()
-    subprocess.check_call(["gcc"] + CFLAGS + ["-o", tmp, SRC, "-lm"])
+    subprocess.check_call(["gcc"] + CFLAGS + EXTRA_CFLAGS + ["-o", tmp, SRC, "-lm"])
     os.replace(tmp, LIB)
     return LIB
 

@@ -44,10 +44,13 @@ def run_bilinear(kind, n=512, M=4, T=800, eta=0.2, noise=0.05, seed=0, record_ev
     G = torch.zeros(M, ld, device=dev)
     wire = plan.new_wire(dev)
     n0 = float(torch.linalg.vector_norm(W[:game.d]))
-    # w_{-1/2} = w_0 and e_0 = 0: the first evaluation points are w_0 - eta g_0
+    # w_{-1/2} = w_0 and e_0 = 0: the first evaluation points are
+    # w_0 - (eta g_0 + e_0), the library's OMD step with q-hat = 0 (w stays w_0)
     G[:, :game.d] = game.operator(W[:game.d].expand(M, -1)) + noise * torch.randn(M, game.d, device=dev,
                                                                                    generator=gen)
-    WX[:, :game.d] = W[:game.d] - eta * G[:, :game.d]
+    Q0 = torch.zeros(ld, device=dev)
+    dqgan.omd_step(plan, eta, Q0, W, G, E, WX)
+    del Q0
     hist = []
     for t in range(1, T + 1):
         G[:, :game.d] = game.operator(WX) + noise * torch.randn(M, game.d, device=dev, generator=gen)
