@@ -453,7 +453,7 @@ __global__ __launch_bounds__(kBlock) void k_fused(const float *__restrict__ G, f
         }
         st_stream(E + rb + i0, cq.enew);
         if constexpr (KIND == kTopk) {
-            store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + tile], i0, cq);
+            store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, topk_tile_base(ta, m, tile), i0, cq);
         } else {
             store_message_rt<KIND, LB>(sign_plane + m * a.sign_words, level_plane + m * a.level_words, val + rb, q, cq,
                                        a.stream_msg != 0);
@@ -557,7 +557,7 @@ __global__ __launch_bounds__(64 * NG) void k_fused_split(const float *__restrict
             }
             st_stream(E + rb + i0, cq.enew);
             if constexpr (KIND == kTopk) {
-                store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + blockIdx.x], i0, cq);
+                store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, topk_tile_base(ta, m, blockIdx.x), i0, cq);
             } else {
                 store_message<KIND, LB, STREAM>(sign_plane + m * a.sign_words, level_plane + m * a.level_words,
                                                 val + rb, q, cq);
@@ -899,7 +899,7 @@ __global__ __launch_bounds__(64) void k_topk_encode_rows(const float *__restrict
     const f32x4 e = ld_stream(E + rb + i0);
     const QuadCodes cq = encode_quad_topk(g, e, a.eta, i0, a.d, rw->T, rw->I);
     st_stream(E + rb + i0, cq.enew);
-    store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, ta.tile_off[m * ta.n_tiles + blockIdx.x], i0, cq);
+    store_topk(val + m * ta.k, ta.idx + m * ta.k, ta.k, topk_tile_base(ta, m, blockIdx.x), i0, cq);
 }
 
 RowArgs row_args(const dqgan_plan_s &P, float eta, uint32_t t) {
@@ -930,7 +930,9 @@ TopkArgs topk_args(const dqgan_plan_s &P, const dqgan_wire &w) {
     if (P.desc.kind == kTopk) {
         ta.rows = P.topk.rows;
         ta.tile_off = P.topk.tile_off;
+        ta.chunk_off = P.topk.chunk_off;
         ta.n_tiles = P.topk.n_tiles;
+        ta.n_chunks = P.topk.n_chunks;
         ta.k = P.desc.k;
         ta.idx = w.idx;
     }
@@ -1106,7 +1108,7 @@ hipError_t launch_topk_apply(const dqgan_plan_s &P, float eta, const float *G, f
 hipError_t launch_topk_encode_rows(const dqgan_plan_s &P, float eta, const float *G, float *E, const dqgan_wire &w,
                                    hipStream_t st) {
     const RowArgs a = row_args(P, eta, 0);
-    TopkArgs ta{P.topk.rows, P.topk.tile_off, P.topk.n_tiles, P.desc.k, w.idx};
+    TopkArgs ta{P.topk.rows, P.topk.tile_off, P.topk.chunk_off, P.topk.n_tiles, P.topk.n_chunks, P.desc.k, w.idx};
     hipLaunchKernelGGL(k_topk_encode_rows, dim3(static_cast<unsigned>(P.topk.n_tiles), static_cast<unsigned>(P.desc.M)),
                        dim3(64), 0, st, G, E, w.val, a, ta);
     return hipGetLastError();

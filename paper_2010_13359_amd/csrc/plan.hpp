@@ -46,45 +46,63 @@ constexpr double kInfinityCacheBytes = 256.0 * 1024 * 1024;
 // key > T, or key == T and i <= I.
 struct TopkRow {
     uint32_t lo, hi;     // candidate band [lo, hi] of keys, from the sample
-    uint32_t n_cand;     // candidates appended by the full pass (may exceed the capacity)
+    uint32_t n_cand;     // candidates staged into the row's list by the full pass (may exceed the capacity)
     uint32_t fallback;   // 1: the band missed the k-th key; the full-row search decides
     uint32_t T, I;       // the selection
-    uint32_t rank;       // full-row search: rank still to place
-    uint32_t kprefix;    // full-row search: key bits decided so far
-    uint32_t iprefix;    // full-row search: ~index bits decided so far
-    uint32_t done;       // full-row search finished early (all ties taken)
+    uint32_t n_spill;    // candidates a wave could not stage: stored from the top of the row's list down
+    uint32_t slots;      // bit p: the candidate search built digit histogram p in this iteration
+    uint32_t n_play;     // candidates still in play after the first key digit, listed for the finish
+    uint32_t pad0;
     uint32_t total;      // selected count found by the tile scan (equals k)
     uint32_t n_above;    // keys above the band, counted by the full pass
     uint32_t pad[4];
 };
 
 constexpr int kTopkTile = 256;            // elements per counting tile (one wave of quads)
+constexpr int kTopkChunkTiles = 64;       // tiles per workgroup of the full pass: one candidate run each
 constexpr int kSampleBins = 32768;        // sample histogram: key >> 16 (keys < 2^31)
 constexpr int64_t kSampleStride = 65536;  // one 256-element chunk sampled per 65536 elements
+constexpr int kDigitBins = 2048;          // radix-select histograms: 11-bit digits
+constexpr int kSelectPasses = 6;          // histogram slots of a search: up to 3 key digits, 3 index digits
 
 // Top-k workspace (one set per plan).
 struct TopkScratch {
     TopkRow *rows = nullptr;        // [M]
-    uint32_t *hist = nullptr;       // [M][kSampleBins] sample histogram; [M][2048] digit histogram
-    uint2 *cand = nullptr;          // [M][cap] (key, index) candidates
+    uint32_t *hist = nullptr;       // [M][kSampleBins] sample histogram (zero between iterations)
+    uint32_t *sel_hist = nullptr;   // [M][kDigitBins] histogram of the first key digit among the candidates
+    uint2 *play = nullptr;          // [M][cap] the candidates in play after the first key digit
+    uint32_t *fb_hist = nullptr;    // [M][kSelectPasses][kDigitBins] digit histograms of the full-row search
+    uint2 *cand = nullptr;          // [M][cap] (key, index) candidates: runs from the bottom, spills from the top
     int64_t cap = 0;
+    uint2 *runs = nullptr;          // [M][n_chunks] (first position, count) of each full-pass workgroup's candidates
     uint32_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per 256-element tile
-    uint32_t *tile_off = nullptr;   // [M][n_tiles] exclusive prefix of tile_cnt
-    uint32_t *chunk_sum = nullptr;  // [M][n_scan_chunks] tile counts per scan chunk
+    uint32_t *tile_off = nullptr;   // [M][n_tiles] selected elements before the tile within its chunk
+    uint32_t *chunk_sum = nullptr;  // [M][n_chunks] selected elements per chunk of kTopkChunkTiles tiles
+    uint32_t *chunk_off = nullptr;  // [M][n_chunks] exclusive prefix of chunk_sum
     uint32_t *agg_start = nullptr;  // [M][n_agg_tiles + 1] first message entry per server-average tile
     int64_t n_agg_tiles = 0;
     int64_t n_tiles = 0;
-    int64_t n_chunks = 0;           // sampled chunks per row
+    int64_t n_chunks = 0;           // chunks of kTopkChunkTiles tiles per row
+    int64_t n_sample_chunks = 0;    // sampled chunks per row
     uint32_t n_samples = 0;         // sampled elements per row
 };
 
+// The state the apply pass reads: the threshold per row and each tile's
+// first output position, tile_off + chunk_off of its chunk.
 struct TopkArgs {
     const TopkRow *rows;
     const uint32_t *tile_off;
+    const uint32_t *chunk_off;
     int64_t n_tiles;
+    int64_t n_chunks;
     int64_t k;
     uint32_t *idx;
 };
+
+__device__ __forceinline__ uint32_t topk_tile_base(const TopkArgs &ta, int m, int64_t tile) {
+    return ta.tile_off[static_cast<int64_t>(m) * ta.n_tiles + tile] +
+           ta.chunk_off[static_cast<int64_t>(m) * ta.n_chunks + tile / kTopkChunkTiles];
+}
 
 }  // namespace dq
 

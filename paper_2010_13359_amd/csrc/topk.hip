@@ -9,16 +9,25 @@
 //  1. sample: one 256-element chunk per 65536 elements, histogram of key>>16;
 //  2. band: the sample ranks k/d * s -+ 8 sigma bracket the k-th key in a
 //     band [lo, hi];
-//  3. full pass: per 256-element tile the number of keys above hi, and every
-//     in-band (key, index) appended to a candidate list;
-//  4. exact radix select of the remaining rank among the candidates (digits
-//     of key - lo, then of ~index when the k-th key is shared) gives T and I;
-//  5. the selected candidates are added to their tiles' counts.
-// If the band missed the k-th key (or the candidates overflow), the row falls
-// back to a full-row radix select over six digits of (key, ~index) (one read
-// of the row per digit) and a recount.  Finally an exclusive scan of the tile
-// counts gives each tile's first output position, which the fused apply
-// pass uses to write (value, index) in ascending index order.
+//  3. full pass: per 256-element tile the number of keys above hi; every
+//     in-band (key, index) goes to a candidate list, each workgroup's as one
+//     contiguous run (its 64 tiles), a tile that overflows its wave's
+//     staging from the top of the list down;
+//  4. exact radix select of the remaining rank among the candidates gives T
+//     and I: the first digit of key - lo from a histogram several workgroups
+//     per row build, the candidates in its bin listed, and the remaining
+//     digits of key - lo (and, when the k-th key is shared and not every
+//     candidate with it is taken, three digits of ~index) decided over that
+//     short list by one workgroup in LDS;
+//  5. selected spilled candidates are added to their tiles' counts; per
+//     64-tile chunk, the selected candidates of its run are added too and
+//     the tiles' offsets within the chunk are scanned; a per-row scan of the
+//     chunk totals gives each chunk's first position.
+// If the band missed the k-th key (or the candidates overflow the list),
+// the row falls back to a full-row radix select over
+// six digits of (key, ~index) (one read of the row per digit) and a recount.
+// The fused apply pass then writes (value, index) in ascending index order
+// from each tile's position.
 #include "device.hpp"
 #include "plan.hpp"
 
@@ -26,18 +35,12 @@ namespace dq {
 
 namespace {
 
-constexpr int kDigitBins = 2048;
-constexpr int kFbBlocks = 128;  // workgroups per row of the full-row search
+constexpr int kFbBlocks = 128;  // workgroups of the full-row search (each looping over the rows)
+constexpr int kSelBlocks = 16;  // workgroups per row of a candidate histogram
 
 __device__ __forceinline__ uint32_t key_of(float g, float e, float eta) {
     const float p = add_rn(mul_rn(eta, g), e);
     return __float_as_uint(p) & 0x7FFFFFFFu;
-}
-
-__global__ __launch_bounds__(kBlock) void k_fill_u32(uint32_t *__restrict__ p, int64_t n, uint32_t v) {
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; i < n;
-         i += static_cast<int64_t>(gridDim.x) * kBlock)
-        p[i] = v;
 }
 
 __global__ __launch_bounds__(kBlock) void k_fill_f32(float *__restrict__ p, int64_t n) {
@@ -84,18 +87,24 @@ __device__ __forceinline__ void add_prefix(int pass, uint32_t bin, uint32_t &kp,
 // largest item (rank >= 1) and the count of items in higher bins.  Returns
 // false if the histogram holds fewer than rank items.
 __device__ bool wave_find_desc(const uint32_t *h, int nb, uint32_t rank, uint32_t &bin, uint32_t &above) {
+    // each lane holds its (at most 32) bins in registers: loaded once, in
+    // parallel, and the lane that holds the rank scans them without reloads
+    constexpr int kMaxPer = kDigitBins / 64;
     const int lane = threadIdx.x & 63;
     const int per = (nb + 63) / 64;
+    uint32_t v[kMaxPer];
     uint32_t s = 0;
-    for (int j = 0; j < per; ++j) {
+#pragma unroll
+    for (int j = 0; j < kMaxPer; ++j) {
         const int b = nb - 1 - (lane * per + j);
-        if (b >= 0) s += h[b];
+        v[j] = (j < per && b >= 0) ? h[b] : 0u;
+        s += v[j];
     }
     uint32_t incl = s;
 #pragma unroll
     for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t v = __shfl_up(incl, o);
-        if (lane >= o) incl += v;
+        const uint32_t x = __shfl_up(incl, o);
+        if (lane >= o) incl += x;
     }
     const uint32_t excl = incl - s;
     const uint64_t hit = __ballot(excl < rank && rank <= incl);
@@ -104,15 +113,16 @@ __device__ bool wave_find_desc(const uint32_t *h, int nb, uint32_t rank, uint32_
     uint32_t rb = 0, ra = 0;
     if (lane == L) {
         uint32_t acc = excl;
-        for (int j = 0; j < per; ++j) {
+        bool found = false;
+#pragma unroll
+        for (int j = 0; j < kMaxPer; ++j) {
             const int b = nb - 1 - (lane * per + j);
-            if (b < 0) break;
-            if (acc + h[b] >= rank) {
+            if (!found && j < per && b >= 0 && acc + v[j] >= rank) {
                 rb = static_cast<uint32_t>(b);
                 ra = acc;
-                break;
+                found = true;
             }
-            acc += h[b];
+            acc += found ? 0u : v[j];
         }
     }
     bin = __shfl(rb, L);
@@ -121,9 +131,12 @@ __device__ bool wave_find_desc(const uint32_t *h, int nb, uint32_t rank, uint32_
 }
 
 // 1. Sample histogram of key >> 16 (one 256-element chunk per 65536 elements).
-// The 128 KiB LDS histogram allows one workgroup per CU, so the workgroup
-// has 16 waves (each loads a chunk) to keep enough scattered loads in flight.
+// The 128 KiB LDS histogram allows one workgroup per CU, so a row has few
+// workgroups (each flushes its nonzero bins with global atomics) and each
+// of their 16 waves keeps four chunks' loads in flight.
 constexpr int kSampleThreads = 1024;
+constexpr int kSampleBlocks = 4;  // workgroups per row
+constexpr int kSampleU = 4;       // chunks in flight per wave
 
 __global__ __launch_bounds__(kSampleThreads) void k_topk_sample(const float *__restrict__ G,
                                                                 const float *__restrict__ E, float eta, int64_t d,
@@ -137,14 +150,27 @@ __global__ __launch_bounds__(kSampleThreads) void k_topk_sample(const float *__r
     const float *g = G + static_cast<int64_t>(m) * ld;
     const float *e = E + static_cast<int64_t>(m) * ld;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int64_t c = static_cast<int64_t>(blockIdx.x) * kWaves + wave; c < n_chunks;
-         c += static_cast<int64_t>(gridDim.x) * kWaves) {
-        const int64_t i0 = c * kSampleStride + 4 * lane;
-        if (i0 < d) {
-            const f32x4 gv = ld4(g + i0), ev = ld4(e + i0);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * kWaves;
+    for (int64_t c0 = static_cast<int64_t>(blockIdx.x) * kWaves + wave; c0 < n_chunks; c0 += stride * kSampleU) {
+        f32x4 gv[kSampleU], ev[kSampleU];
 #pragma unroll
-            for (int k = 0; k < 4; ++k)
-                if (i0 + k < d) atomicAdd(&h[key_of(elem(gv, k), elem(ev, k), eta) >> 16], 1u);
+        for (int u = 0; u < kSampleU; ++u) {
+            // chunks past the row's last are not examined; their loads read
+            // the first chunk (always in bounds)
+            const int64_t c = c0 + stride * u;
+            const int64_t i0 = (c < n_chunks ? c * kSampleStride : 0) + 4 * lane;
+            gv[u] = ld4(g + i0);
+            ev[u] = ld4(e + i0);
+        }
+#pragma unroll
+        for (int u = 0; u < kSampleU; ++u) {
+            const int64_t c = c0 + stride * u;
+            const int64_t i0 = c * kSampleStride + 4 * lane;
+            if (c < n_chunks && i0 < d) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    if (i0 + k < d) atomicAdd(&h[key_of(elem(gv[u], k), elem(ev[u], k), eta) >> 16], 1u);
+            }
         }
     }
     __syncthreads();
@@ -176,8 +202,9 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *w
 
 // 2. Band: the sample ranks k/d * s -+ 8 sigma (binomial) bracket the k-th
 // key; the bins where the count from the top reaches them bound [lo, hi].
-__global__ __launch_bounds__(1024) void k_topk_band(const uint32_t *__restrict__ hist, TopkRow *__restrict__ rows,
-                                                    uint32_t n_samples, int64_t d, int64_t k) {
+__global__ __launch_bounds__(1024) void k_topk_band(uint32_t *__restrict__ hist, uint32_t *__restrict__ sel_hist,
+                                                    TopkRow *__restrict__ rows, uint32_t n_samples, int64_t d,
+                                                    int64_t k) {
     // thread t holds the t-th group of kPer bins counted from the top; a
     // block scan finds the group where the count from the top reaches a
     // rank, and that thread finds the bin in its registers.
@@ -197,6 +224,12 @@ __global__ __launch_bounds__(1024) void k_topk_band(const uint32_t *__restrict__
         asc[4 * q + 2] = v.z;
         asc[4 * q + 3] = v.w;
     }
+    // the histogram is zeroed once read (the next iteration's sample starts
+    // from zero), and so are the row's candidate digit histograms
+    uint4 *dst = reinterpret_cast<uint4 *>(hist + static_cast<int64_t>(m) * kSampleBins + kSampleBins - kPer * (t + 1));
+#pragma unroll
+    for (int q = 0; q < kPer / 4; ++q) dst[q] = make_uint4(0u, 0u, 0u, 0u);
+    for (int b = t; b < kDigitBins; b += 1024) sel_hist[static_cast<int64_t>(m) * kDigitBins + b] = 0u;
     uint32_t s = 0;
 #pragma unroll
     for (int j = 0; j < kPer; ++j) s += asc[j];
@@ -249,9 +282,12 @@ __global__ __launch_bounds__(1024) void k_topk_band(const uint32_t *__restrict__
 // 16 counts with one 64-byte store at the end: over 64 rows of 10^8 elements
 // a 4-byte count store per tile held the pass 8 % above its loads alone.
 // Candidates are staged in the wave's quarter of an LDS buffer with a
-// wave-uniform count (a wave whose quarter overflows appends straight to the
-// row's list); at the end the workgroup adds its above-band total and its
-// staged candidates to the row with one atomic each.  A tile wholly below d
+// wave-uniform count; at the end the workgroup adds its above-band total to
+// the row and writes its candidates as one run from the bottom of the row's
+// list, whose place it records for the per-chunk count.  A tile whose
+// candidates do not fit the wave's quarter (more than 256 in-band keys in
+// its 4096 elements: a segment whose scale puts most of it in the band)
+// stores them from the top of the list down ("spills").  A tile wholly below d
 // (all but the last of a row) is classified without per-element bounds
 // tests, on masks taken straight from the comparisons.
 constexpr int kPassRounds = 4;
@@ -260,7 +296,8 @@ constexpr int kPassTilesPerBlock = kPassTilesPerWave * (kBlock / 64);
 __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                       TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
-                                                      uint2 *__restrict__ cand, int64_t cap) {
+                                                      uint2 *__restrict__ cand, int64_t cap, uint2 *__restrict__ runs,
+                                                      int64_t n_chunks) {
     constexpr uint32_t kStage = 256;  // staged candidates per wave
     constexpr int kWaves = kBlock / 64;
     __shared__ uint2 buf[kWaves][kStage];
@@ -340,14 +377,16 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                     }
                     ns += tot;
                 } else {
-                    uint32_t gbase = 0;
-                    if (lane == 0) gbase = atomicAdd(&rows[m].n_cand, tot);
-                    gbase = __builtin_amdgcn_readfirstlane(gbase);
+                    // the wave's staging is full: these go to the top of the
+                    // row's list, counted per tile by k_topk_spill_count
+                    uint32_t sbase = 0;
+                    if (lane == 0) sbase = atomicAdd(&rows[m].n_spill, tot);
+                    sbase = __builtin_amdgcn_readfirstlane(sbase);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
                         if ((cb[k] >> lane) & 1u) {
-                            const int64_t pos = static_cast<int64_t>(gbase) + pre;
-                            if (pos < cap) crow[pos] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                            const int64_t j = static_cast<int64_t>(sbase) + pre;
+                            if (j < cap) crow[cap - 1 - j] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
                             ++pre;
                         }
                     }
@@ -371,6 +410,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
         }
         if (a) atomicAdd(&rows[m].n_above, a);
         base = n ? atomicAdd(&rows[m].n_cand, n) : 0u;
+        runs[static_cast<int64_t>(m) * n_chunks + blockIdx.x] = make_uint2(base, n);
     }
     __syncthreads();
     uint32_t off = base;
@@ -381,298 +421,487 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     }
 }
 
-// 4. Exact selection among the candidates (one workgroup per row).  Rows
-// whose band missed are handed to the full-row search.  The candidates' keys
-// lie in [lo, hi]: the digits are taken over key - lo, 11 bits at a time from
-// the top of its width, then (only if the k-th key is shared and not every
-// tie is taken) over ~index.
-constexpr int kSelU = 8;  // candidates in flight per thread in the selection passes
+// 4. Exact selection among the candidates.  A row's search is on when its
+// candidates hold the k-th key: all staged, within the list, and the keys
+// above the band fewer than k with the rest of k among the candidates.
+__device__ __forceinline__ uint64_t n_listed(const TopkRow &r) {
+    return static_cast<uint64_t>(r.n_cand) + r.n_spill;
+}
+__device__ __forceinline__ bool sel_ok(const TopkRow &r, int64_t k, int64_t cap) {
+    return n_listed(r) <= static_cast<uint64_t>(cap) && r.n_above < static_cast<uint64_t>(k) &&
+           static_cast<uint64_t>(k) - r.n_above <= n_listed(r);
+}
+// Candidate j of a row's list: the runs [0, n_cand), then the spills stored
+// from the top down.
+__device__ __forceinline__ uint2 cand_at(const uint2 *__restrict__ crow, uint64_t j, uint32_t n_cand, int64_t cap) {
+    return crow[j < n_cand ? j : static_cast<uint64_t>(cap) - 1 - (j - n_cand)];
+}
 
-__global__ __launch_bounds__(1024) void k_topk_select(TopkRow *__restrict__ rows, const uint2 *__restrict__ cand,
-                                                      int64_t cap, int64_t k, uint32_t *__restrict__ hist) {
-    __shared__ uint32_t h[kDigitBins];
-    __shared__ uint32_t res[3];
-    const int m = blockIdx.x;
-    const int tid = threadIdx.x;
-    const uint32_t n_cand = rows[m].n_cand;
-    const uint64_t n_above = rows[m].n_above;
-    const bool ok = n_cand <= cap && n_above < static_cast<uint64_t>(k) &&
-                    static_cast<uint64_t>(k) - n_above <= n_cand;
-    if (!ok) {
-        if (tid == 0) {
-            rows[m].fallback = 1u;
-            rows[m].rank = static_cast<uint32_t>(k);
-            rows[m].kprefix = 0u;
-            rows[m].iprefix = 0u;
-            rows[m].done = 0u;
-        }
-        uint32_t *hm = hist + static_cast<int64_t>(m) * kDigitBins;
-        for (int b = tid; b < kDigitBins; b += 1024) hm[b] = 0u;
-        return;
-    }
-    uint32_t rank = static_cast<uint32_t>(static_cast<uint64_t>(k) - n_above);
-    const uint32_t lo = rows[m].lo, span = rows[m].hi - lo;
+// The search over the candidates: the first digit of key - lo (its top 11
+// bits, or all of them when narrower) from a histogram that kSelBlocks
+// workgroups per row build over the whole list; the candidates in that
+// digit's bin -- a few hundred or thousand in a typical row -- are then
+// listed once, and one workgroup per row decides the remaining digits of
+// key - lo and, when the k-th key is shared and not every candidate with it
+// is taken, three digits of ~index, all in LDS over that list.
+struct TopState {
+    uint32_t rank;   // rank still to place among the candidates in play
+    uint32_t kp;     // decided high bits of key - lo
+    int top;         // bits of key - lo not yet decided
+};
+
+__device__ __forceinline__ int key_width(const TopkRow &r) {
+    const uint32_t span = r.hi - r.lo;
     int width = 0;
     while (width < 32 && (span >> width) != 0u) ++width;  // bits of key - lo
+    return width;
+}
+
+// The state after the first digit (one wave replays it from the histogram).
+__device__ TopState sel_first_digit(const TopkRow &r, int64_t k, const uint32_t *__restrict__ h) {
+    TopState s;
+    s.rank = static_cast<uint32_t>(static_cast<uint64_t>(k) - r.n_above);
+    s.kp = 0u;
+    s.top = key_width(r);
+    if (s.top > 0) {
+        const int wbits = s.top < 11 ? s.top : 11;
+        const int shift = s.top - wbits;
+        uint32_t bin = 0, above = 0;
+        wave_find_desc(h, 1 << wbits, s.rank, bin, above);
+        s.rank -= above;
+        s.kp = bin << shift;
+        s.top = shift;
+    }
+    return s;
+}
+
+constexpr int kSelU = 8;  // candidates in flight per thread
+
+// The first key digit's histogram (kSelBlocks workgroups per row).
+__global__ __launch_bounds__(kBlock) void k_topk_sel_top(const TopkRow *__restrict__ rows,
+                                                         const uint2 *__restrict__ cand, int64_t cap, int64_t k,
+                                                         uint32_t *__restrict__ sel_hist) {
+    __shared__ uint32_t h[kDigitBins];
+    const int m = blockIdx.y;
+    const TopkRow r = rows[m];
+    const int width = key_width(r);
+    if (!sel_ok(r, k, cap) || width == 0) return;
+    const int wbits = width < 11 ? width : 11;
+    const int shift = width - wbits;
+    const int nb = 1 << wbits;
+    for (int b = threadIdx.x; b < nb; b += kBlock) h[b] = 0u;
+    __syncthreads();
     const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-    // key digits
-    uint32_t kp = 0;  // decided high bits of key - lo
-    int top = width;
-    uint32_t n_bin = n_cand;
+    const uint64_t n = n_listed(r);
+    const uint64_t per = (n + kSelBlocks - 1) / kSelBlocks;
+    const uint64_t j_lo = per * blockIdx.x, j_hi = j_lo + per < n ? j_lo + per : n;
+    for (uint64_t j0 = j_lo + threadIdx.x; j0 < j_hi; j0 += static_cast<uint64_t>(kBlock) * kSelU) {
+        uint32_t keys[kSelU];
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) {
+            const uint64_t j = j0 + static_cast<uint64_t>(kBlock) * u;
+            keys[u] = j < j_hi ? cand_at(crow, j, r.n_cand, cap).x : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u)
+            if (j0 + static_cast<uint64_t>(kBlock) * u < j_hi) atomicAdd(&h[(keys[u] - r.lo) >> shift], 1u);
+    }
+    __syncthreads();
+    uint32_t *hm = sel_hist + static_cast<int64_t>(m) * kDigitBins;
+    for (int b = threadIdx.x; b < nb; b += kBlock)
+        if (h[b]) atomicAdd(&hm[b], h[b]);
+}
+
+// The candidates in the first digit's bin, listed (kSelBlocks workgroups per
+// row; one atomic per wave and round).
+__global__ __launch_bounds__(kBlock) void k_topk_sel_collect(TopkRow *__restrict__ rows,
+                                                             const uint2 *__restrict__ cand, int64_t cap, int64_t k,
+                                                             const uint32_t *__restrict__ sel_hist,
+                                                             uint2 *__restrict__ play) {
+    __shared__ TopState st;
+    const int m = blockIdx.y;
+    const TopkRow r = rows[m];
+    if (!sel_ok(r, k, cap)) return;
+    if (threadIdx.x < 64) {
+        const TopState s = sel_first_digit(r, k, sel_hist + static_cast<int64_t>(m) * kDigitBins);
+        if (threadIdx.x == 0) st = s;
+    }
+    __syncthreads();
+    const TopState s = st;
+    const int lane = threadIdx.x & 63;
+    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    uint2 *prow = play + static_cast<int64_t>(m) * cap;
+    const uint64_t n = n_listed(r);
+    const uint64_t per = (n + kSelBlocks - 1) / kSelBlocks;
+    const uint64_t j_lo = per * blockIdx.x, j_hi = j_lo + per < n ? j_lo + per : n;
+    // rounds of kSelU * kBlock candidates (all loaded before the first is
+    // examined; every thread of the workgroup in each round), one atomic per
+    // wave and round
+    for (uint64_t jb = j_lo; jb < j_hi; jb += static_cast<uint64_t>(kBlock) * kSelU) {
+        uint2 cs[kSelU];
+        uint64_t mask[kSelU];
+        uint32_t tot = 0;
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) {
+            const uint64_t j = jb + static_cast<uint64_t>(kBlock) * u + threadIdx.x;
+            cs[u] = j < j_hi ? cand_at(crow, j, r.n_cand, cap) : make_uint2(0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) {
+            const uint64_t j = jb + static_cast<uint64_t>(kBlock) * u + threadIdx.x;
+            const uint32_t rel = cs[u].x - r.lo;
+            mask[u] = __ballot(j < j_hi && (s.top >= 32 || (rel >> s.top) == (s.kp >> s.top)));
+            tot += __popcll(mask[u]);
+        }
+        if (tot) {
+            uint32_t base = 0;
+            if (lane == 0) base = atomicAdd(&rows[m].n_play, tot);
+            base = __builtin_amdgcn_readfirstlane(base);
+#pragma unroll
+            for (int u = 0; u < kSelU; ++u) {
+                if ((mask[u] >> lane) & 1u) {
+                    const uint32_t at = base + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask[u] >> 32),
+                                                                         __builtin_amdgcn_mbcnt_lo(
+                                                                             static_cast<uint32_t>(mask[u]), 0u));
+                    if (at < cap) prow[at] = cs[u];
+                }
+                base += static_cast<uint32_t>(__popcll(mask[u]));
+            }
+        }
+    }
+}
+
+// The search's result (one workgroup per row): the remaining digits of
+// key - lo and, if needed, of ~index over the listed candidates; or the
+// hand-over of the row to the full-row search (whose digit histograms are
+// zeroed here).
+__device__ __forceinline__ void block_find(const uint32_t *h, int nb, uint32_t rank, uint32_t *res) {
+    if (threadIdx.x < 64) {
+        uint32_t bin = 0, above = 0;
+        wave_find_desc(h, nb, rank, bin, above);
+        if (threadIdx.x == 0) {
+            res[0] = bin;
+            res[1] = above;
+            res[2] = h[bin];
+        }
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(1024) void k_topk_sel_finish(TopkRow *__restrict__ rows, int64_t cap, int64_t k,
+                                                          const uint32_t *__restrict__ sel_hist,
+                                                          const uint2 *__restrict__ play,
+                                                          uint32_t *__restrict__ fb_hist) {
+    __shared__ uint32_t h[kDigitBins];
+    __shared__ TopState st;
+    __shared__ uint32_t res[3];
+    const int m = blockIdx.x;
+    const TopkRow r = rows[m];
+    if (!sel_ok(r, k, cap)) {
+        uint32_t *f6 = fb_hist + static_cast<int64_t>(m) * kSelectPasses * kDigitBins;
+        for (int b = threadIdx.x; b < kSelectPasses * kDigitBins; b += 1024) f6[b] = 0u;
+        if (threadIdx.x == 0) rows[m].fallback = 1u;
+        return;
+    }
+    if (threadIdx.x < 64) {
+        const TopState s = sel_first_digit(r, k, sel_hist + static_cast<int64_t>(m) * kDigitBins);
+        if (threadIdx.x == 0) st = s;
+    }
+    __syncthreads();
+    uint32_t rank = st.rank, kp = st.kp;
+    int top = st.top;
+    const uint2 *prow = play + static_cast<int64_t>(m) * cap;
+    const uint32_t n = r.n_play < cap ? r.n_play : static_cast<uint32_t>(cap);
+    uint32_t n_bin = n;
+    // remaining digits of key - lo
     while (top > 0) {
         const int wbits = top < 11 ? top : 11;
         const int shift = top - wbits;
-        const uint32_t dmask = (1u << wbits) - 1u;
         const int nb = 1 << wbits;
-        for (int b = tid; b < nb; b += 1024) h[b] = 0u;
+        for (int b = threadIdx.x; b < nb; b += 1024) h[b] = 0u;
         __syncthreads();
-        // kSelU candidates per thread per trip, all loads issued before use
-        for (uint64_t j0 = tid; j0 < n_cand; j0 += 1024 * kSelU) {
-            uint32_t keys[kSelU];
-#pragma unroll
-            for (int u = 0; u < kSelU; ++u) {
-                const uint64_t j = j0 + 1024u * u;
-                keys[u] = j < n_cand ? crow[j].x : 0u;
-            }
-#pragma unroll
-            for (int u = 0; u < kSelU; ++u) {
-                const uint32_t rel = keys[u] - lo;
-                const bool play = j0 + 1024u * u < n_cand && (top >= 32 || (rel >> top) == (kp >> top));
-                if (play) atomicAdd(&h[(rel >> shift) & dmask], 1u);
-            }
+        for (uint32_t j = threadIdx.x; j < n; j += 1024) {
+            const uint32_t rel = prow[j].x - r.lo;
+            if (top >= 32 || (rel >> top) == (kp >> top)) atomicAdd(&h[(rel >> shift) & (nb - 1)], 1u);
         }
         __syncthreads();
-        if (tid < 64) {
-            uint32_t bin = 0, above = 0;
-            wave_find_desc(h, nb, rank, bin, above);
-            if (tid == 0) {
-                res[0] = bin;
-                res[1] = above;
-                res[2] = h[bin];
-            }
-        }
-        __syncthreads();
+        block_find(h, nb, rank, res);
         rank -= res[1];
         kp |= res[0] << shift;
         n_bin = res[2];
         top = shift;
         __syncthreads();
     }
-    const uint32_t T = lo + kp;
-    uint32_t ip = 0, I = 0xFFFFFFFFu;
+    const uint32_t T = r.lo + kp;
+    uint32_t I = 0xFFFFFFFFu;
     if (rank != n_bin) {
-        // index digits among the ties at T (composite order: smaller index first)
+        // the k-th key is shared and not all of its candidates are taken:
+        // three digits of ~index among them (smaller index first)
+        uint32_t ip = 0u;
         for (int pass = 3; pass < 6; ++pass) {
             const int nb = bins_of(pass);
-            for (int b = tid; b < nb; b += 1024) h[b] = 0u;
+            for (int b = threadIdx.x; b < nb; b += 1024) h[b] = 0u;
             __syncthreads();
-            for (uint64_t j0 = tid; j0 < n_cand; j0 += 1024 * kSelU) {
-                uint2 cs[kSelU];
-#pragma unroll
-                for (int u = 0; u < kSelU; ++u) {
-                    const uint64_t j = j0 + 1024u * u;
-                    cs[u] = j < n_cand ? crow[j] : make_uint2(0u, 0u);
-                }
-#pragma unroll
-                for (int u = 0; u < kSelU; ++u) {
-                    const uint32_t ni = ~cs[u].y;
-                    if (j0 + 1024u * u < n_cand && in_play(pass, cs[u].x, ni, T, ip))
-                        atomicAdd(&h[digit_of(pass, cs[u].x, ni)], 1u);
-                }
+            for (uint32_t j = threadIdx.x; j < n; j += 1024) {
+                const uint2 c = prow[j];
+                const uint32_t ni = ~c.y;
+                if (in_play(pass, c.x, ni, T, ip)) atomicAdd(&h[digit_of(pass, c.x, ni)], 1u);
             }
             __syncthreads();
-            if (tid < 64) {
-                uint32_t bin = 0, above = 0;
-                wave_find_desc(h, nb, rank, bin, above);
-                if (tid == 0) {
-                    res[0] = bin;
-                    res[1] = above;
-                }
-            }
-            __syncthreads();
+            block_find(h, nb, rank, res);
+            uint32_t kd = 0;
             rank -= res[1];
-            uint32_t kdummy = 0;
-            add_prefix(pass, res[0], kdummy, ip);
+            add_prefix(pass, res[0], kd, ip);
             __syncthreads();
         }
         I = ~ip;
     }
-    if (tid == 0) {
+    if (threadIdx.x == 0) {
         rows[m].T = T;
         rows[m].I = I;
     }
 }
 
-// 5. Add the selected candidates to their tiles' counts.
-__global__ __launch_bounds__(kBlock) void k_topk_count(const TopkRow *__restrict__ rows, const uint2 *__restrict__ cand,
-                                                       int64_t cap, uint32_t *__restrict__ tile_cnt, int64_t n_tiles) {
-    const int m = blockIdx.y;
-    const TopkRow r = rows[m];
-    if (r.fallback) return;
-    const uint32_t n = r.n_cand;
-    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-    uint32_t *trow = tile_cnt + static_cast<int64_t>(m) * n_tiles;
-    const int64_t step = static_cast<int64_t>(gridDim.x) * kBlock;
-    // kSelU candidates per thread per trip, all loads issued before use
-    for (int64_t j0 = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j0 < n; j0 += step * kSelU) {
-        uint2 cs[kSelU];
-#pragma unroll
-        for (int u = 0; u < kSelU; ++u) {
-            const int64_t j = j0 + step * u;
-            cs[u] = j < n ? crow[j] : make_uint2(0u, 0u);
-        }
-#pragma unroll
-        for (int u = 0; u < kSelU; ++u) {
-            const uint2 c = cs[u];
-            if (j0 + step * u < n && (c.x > r.T || (c.x == r.T && c.y <= r.I))) atomicAdd(&trow[c.y >> 8], 1u);
-        }
-    }
+// 6. Full-row search of a row whose band missed: six digits of (key, ~index)
+// over the whole row, one histogram slot per digit.  The kernels loop over
+// the rows (a 1-D grid of kFbBlocks workgroups), so that when no row falls
+// back -- the usual case -- each launch is a short loop over the row flags.
+constexpr int kMaxRows = 1024;  // the library's largest worker count
+
+// The rows that fell back, gathered into LDS by the whole workgroup with one
+// parallel read of the flags (the order does not matter: rows are
+// independent).  Returns their number.
+__device__ int gather_fallback_rows(const TopkRow *__restrict__ rows, int M, int *fb_rows, int *n_fb) {
+    if (threadIdx.x == 0) *n_fb = 0;
+    __syncthreads();
+    for (int m = threadIdx.x; m < M; m += kBlock)
+        if (rows[m].fallback) fb_rows[atomicAdd(n_fb, 1)] = m;
+    __syncthreads();
+    return *n_fb;
 }
 
-// 6. Full-row search of a row whose band missed: histogram of one digit ...
-__global__ __launch_bounds__(kBlock) void k_topk_fb_hist(int pass, const float *__restrict__ G,
-                                                         const float *__restrict__ E, float eta, int64_t d, int64_t ld,
-                                                         const TopkRow *__restrict__ rows,
-                                                         uint32_t *__restrict__ hist) {
-    __shared__ uint32_t h[kDigitBins];
-    const int m = blockIdx.y;
-    const TopkRow r = rows[m];
-    if (!r.fallback || r.done) return;
-    const int nb = bins_of(pass);
-    for (int b = threadIdx.x; b < nb; b += kBlock) h[b] = 0u;
-    __syncthreads();
-    const float *g = G + static_cast<int64_t>(m) * ld;
-    const float *e = E + static_cast<int64_t>(m) * ld;
-    const int64_t nq = (d + 3) / 4;
-    for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nq;
-         q += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const f32x4 gv = ld4(g + 4 * q), ev = ld4(e + 4 * q);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int64_t i = 4 * q + k;
-            if (i < d) {
-                const uint32_t key = key_of(elem(gv, k), elem(ev, k), eta);
-                const uint32_t ni = ~static_cast<uint32_t>(i);
-                if (in_play(pass, key, ni, r.kprefix, r.iprefix)) atomicAdd(&h[digit_of(pass, key, ni)], 1u);
+struct FbState {
+    uint32_t rank, kprefix, iprefix, T, I;
+    int next;  // the digit whose histogram comes next, or kSelectPasses when decided
+};
+
+__device__ FbState fb_replay(int64_t k, const uint32_t *__restrict__ f6, int upto) {
+    FbState s{static_cast<uint32_t>(k), 0u, 0u, 0u, 0xFFFFFFFFu, 0};
+    for (int pass = 0; pass < kSelectPasses; ++pass) {
+        if (pass >= upto) {
+            s.next = pass;
+            return s;
+        }
+        uint32_t bin = 0, above = 0;
+        wave_find_desc(f6 + pass * kDigitBins, bins_of(pass), s.rank, bin, above);
+        const uint32_t n_bin = f6[pass * kDigitBins + bin];
+        s.rank -= above;
+        add_prefix(pass, bin, s.kprefix, s.iprefix);
+        if (pass == 2) {
+            s.T = s.kprefix;
+            if (s.rank == n_bin) {  // every element with key T is taken
+                s.next = kSelectPasses;
+                return s;
             }
         }
+        if (pass == 5) s.I = ~s.iprefix;
     }
-    __syncthreads();
-    uint32_t *hm = hist + static_cast<int64_t>(m) * kDigitBins;
-    for (int b = threadIdx.x; b < nb; b += kBlock)
-        if (h[b]) atomicAdd(&hm[b], h[b]);
+    s.next = kSelectPasses;
+    return s;
 }
 
-// ... then place the rank in it (one wave per row).
-__global__ __launch_bounds__(64) void k_topk_fb_digit(int pass, TopkRow *__restrict__ rows,
-                                                      uint32_t *__restrict__ hist) {
-    const int m = blockIdx.x;
-    TopkRow r = rows[m];
-    if (!r.fallback || r.done) return;
-    uint32_t *hm = hist + static_cast<int64_t>(m) * kDigitBins;
-    const int nb = bins_of(pass);
-    uint32_t bin = 0, above = 0;
-    wave_find_desc(hm, nb, r.rank, bin, above);
-    const uint32_t n_bin = hm[bin];
-    __syncthreads();
-    for (int b = threadIdx.x; b < kDigitBins; b += 64) hm[b] = 0u;
-    if (threadIdx.x == 0) {
-        r.rank -= above;
-        add_prefix(pass, bin, r.kprefix, r.iprefix);
-        if (pass == 2 && r.rank == n_bin) {
-            r.T = r.kprefix;
-            r.I = 0xFFFFFFFFu;
-            r.done = 1u;
-        } else if (pass == 2) {
-            r.T = r.kprefix;
-        } else if (pass == 5) {
-            r.I = ~r.iprefix;
-            r.done = 1u;
+__global__ __launch_bounds__(kBlock) void k_topk_fb_hist(int pass, const float *__restrict__ G,
+                                                         const float *__restrict__ E, float eta, int64_t d, int64_t ld,
+                                                         int32_t M, int64_t k, const TopkRow *__restrict__ rows,
+                                                         uint32_t *__restrict__ fb_hist) {
+    __shared__ uint32_t h[kDigitBins];
+    __shared__ FbState st;
+    __shared__ int fb_rows[kMaxRows];
+    __shared__ int n_fb;
+    const int nf = gather_fallback_rows(rows, M, fb_rows, &n_fb);
+    for (int q = 0; q < nf; ++q) {
+        const int m = fb_rows[q];
+        uint32_t *f6 = fb_hist + static_cast<int64_t>(m) * kSelectPasses * kDigitBins;
+        if (threadIdx.x < 64) {
+            const FbState s = fb_replay(k, f6, pass);
+            if (threadIdx.x == 0) st = s;
         }
-        rows[m] = r;
+        __syncthreads();
+        const FbState s = st;
+        if (s.next == pass) {
+            const int nb = bins_of(pass);
+            for (int b = threadIdx.x; b < nb; b += kBlock) h[b] = 0u;
+            __syncthreads();
+            const float *g = G + static_cast<int64_t>(m) * ld;
+            const float *e = E + static_cast<int64_t>(m) * ld;
+            const int64_t nq = (d + 3) / 4;
+            for (int64_t q = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; q < nq;
+                 q += static_cast<int64_t>(gridDim.x) * kBlock) {
+                const f32x4 gv = ld4(g + 4 * q), ev = ld4(e + 4 * q);
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int64_t i = 4 * q + c;
+                    if (i < d) {
+                        const uint32_t key = key_of(elem(gv, c), elem(ev, c), eta);
+                        const uint32_t ni = ~static_cast<uint32_t>(i);
+                        if (in_play(pass, key, ni, s.kprefix, s.iprefix)) atomicAdd(&h[digit_of(pass, key, ni)], 1u);
+                    }
+                }
+            }
+            __syncthreads();
+            for (int b = threadIdx.x; b < nb; b += kBlock)
+                if (h[b]) atomicAdd(&f6[pass * kDigitBins + b], h[b]);
+        }
+        __syncthreads();  // st and h are reused for the next row
     }
 }
 
-// ... and count the selection per tile.
+// ... then the selection of each fallen-back row per tile (and T, I).
 __global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restrict__ G, const float *__restrict__ E,
                                                             float eta, int64_t d, int64_t ld, int64_t n_tiles,
-                                                            const TopkRow *__restrict__ rows,
+                                                            int32_t M, int64_t k, TopkRow *__restrict__ rows,
+                                                            const uint32_t *__restrict__ fb_hist,
                                                             uint32_t *__restrict__ tile_cnt) {
+    __shared__ FbState st;
+    __shared__ int fb_rows[kMaxRows];
+    __shared__ int n_fb;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nf = gather_fallback_rows(rows, M, fb_rows, &n_fb);
+    for (int q = 0; q < nf; ++q) {
+        const int m = fb_rows[q];
+        if (threadIdx.x < 64) {
+            const FbState s = fb_replay(k, fb_hist + static_cast<int64_t>(m) * kSelectPasses * kDigitBins,
+                                        kSelectPasses);
+            if (threadIdx.x == 0) st = s;
+        }
+        __syncthreads();
+        const FbState s = st;
+        if (blockIdx.x == 0 && threadIdx.x == 0) {
+            rows[m].T = s.T;
+            rows[m].I = s.I;
+        }
+        const float *g = G + static_cast<int64_t>(m) * ld;
+        const float *e = E + static_cast<int64_t>(m) * ld;
+        for (int64_t tile = static_cast<int64_t>(blockIdx.x) * 4 + wave; tile < n_tiles;
+             tile += static_cast<int64_t>(gridDim.x) * 4) {
+            const int64_t i0 = tile * kTopkTile + 4 * lane;
+            const f32x4 gv = ld4(g + i0), ev = ld4(e + i0);
+            uint32_t n = 0;
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+                const int64_t i = i0 + c;
+                const uint32_t key = key_of(elem(gv, c), elem(ev, c), eta);
+                const bool sel = i < d && (key > s.T || (key == s.T && static_cast<uint32_t>(i) <= s.I));
+                n += __popcll(__ballot(sel));
+            }
+            if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = n;
+        }
+        __syncthreads();  // st is reused for the next row
+    }
+}
+
+// Spilled candidates (stored from the top of the list) added to their tiles'
+// counts, for rows whose candidate search decided; nothing to do for most
+// rows (a short exit).
+constexpr int kSpillBlocks = 16;  // workgroups per row
+
+__global__ __launch_bounds__(kBlock) void k_topk_spill_count(const TopkRow *__restrict__ rows,
+                                                             const uint2 *__restrict__ cand, int64_t cap,
+                                                             uint32_t *__restrict__ tile_cnt, int64_t n_tiles) {
     const int m = blockIdx.y;
     const TopkRow r = rows[m];
-    if (!r.fallback) return;
+    if (r.fallback || r.n_spill == 0) return;
+    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    uint32_t *trow = tile_cnt + static_cast<int64_t>(m) * n_tiles;
+    const int64_t n = r.n_spill;  // at most cap - n_cand (the search decided)
+    for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n;
+         j += static_cast<int64_t>(gridDim.x) * kBlock) {
+        const uint2 c = crow[cap - 1 - j];
+        if (c.x > r.T || (c.x == r.T && c.y <= r.I)) atomicAdd(&trow[c.y / kTopkTile], 1u);
+    }
+}
+
+// 7. Per chunk of kTopkChunkTiles tiles (one wave; four chunks per
+// workgroup, independent): the selected candidates of the chunk's run added
+// to its tiles' counts, the tiles' offsets within the chunk (exclusive
+// scan) and the chunk's total.  A fallen-back row's counts come whole from
+// the recount.
+__global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__restrict__ rows,
+                                                            const uint2 *__restrict__ cand, int64_t cap,
+                                                            const uint2 *__restrict__ runs,
+                                                            const uint32_t *__restrict__ tile_cnt,
+                                                            uint32_t *__restrict__ tile_off,
+                                                            uint32_t *__restrict__ chunk_sum, int64_t n_tiles,
+                                                            int64_t n_chunks) {
+    __shared__ uint32_t sel_all[kBlock / 64][kTopkChunkTiles];
+    const int m = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const float *g = G + static_cast<int64_t>(m) * ld;
-    const float *e = E + static_cast<int64_t>(m) * ld;
-    for (int64_t tile = static_cast<int64_t>(blockIdx.x) * 4 + wave; tile < n_tiles;
-         tile += static_cast<int64_t>(gridDim.x) * 4) {
-        const int64_t i0 = tile * kTopkTile + 4 * lane;
-        const f32x4 gv = ld4(g + i0), ev = ld4(e + i0);
-        uint32_t n = 0;
+    const int64_t c = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave;
+    if (c >= n_chunks) return;  // whole waves: no barrier below spans waves
+    uint32_t *sel = sel_all[wave];
+    const int64_t t = c * kTopkChunkTiles + lane;
+    const TopkRow r = rows[m];
+    uint32_t cnt = t < n_tiles ? tile_cnt[static_cast<int64_t>(m) * n_tiles + t] : 0u;
+    if (!r.fallback) {
+        sel[lane] = 0u;
+        __builtin_amdgcn_wave_barrier();
+        const uint2 run = runs[static_cast<int64_t>(m) * n_chunks + c];
+        const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+        const int64_t first_tile = c * kTopkChunkTiles;
+        // up to 8 of the lane's candidates loaded at once (a run holds at
+        // most 1024)
+        constexpr int kRunU = 8;
+        for (uint32_t j0 = lane; j0 < run.y; j0 += 64 * kRunU) {
+            uint2 cd[kRunU];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const int64_t i = i0 + k;
-            const uint32_t key = key_of(elem(gv, k), elem(ev, k), eta);
-            const bool sel = i < d && (key > r.T || (key == r.T && static_cast<uint32_t>(i) <= r.I));
-            n += __popcll(__ballot(sel));
+            for (int u = 0; u < kRunU; ++u) {
+                const uint32_t j = j0 + 64 * u;
+                const int64_t pos = static_cast<int64_t>(run.x) + j;
+                cd[u] = (j < run.y && pos < cap) ? crow[pos] : make_uint2(0u, 0xFFFFFFFFu);
+            }
+#pragma unroll
+            for (int u = 0; u < kRunU; ++u) {
+                if (j0 + 64 * u >= run.y) continue;
+                if (cd[u].x > r.T || (cd[u].x == r.T && cd[u].y <= r.I)) {
+                    const int64_t lt = static_cast<int64_t>(cd[u].y / kTopkTile) - first_tile;
+                    if (lt >= 0 && lt < kTopkChunkTiles) atomicAdd(&sel[lt], 1u);
+                }
+            }
         }
-        if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = n;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        cnt += sel[lane];
     }
+    uint32_t incl = cnt;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t v = __shfl_up(incl, o);
+        if (lane >= o) incl += v;
+    }
+    if (t < n_tiles) tile_off[static_cast<int64_t>(m) * n_tiles + t] = incl - cnt;
+    if (lane == 63) chunk_sum[static_cast<int64_t>(m) * n_chunks + c] = incl;
 }
 
-// 7. Exclusive scan of the tile counts of each row, in chunks of 4096 tiles:
-// each workgroup scans its chunk (4 consecutive counts per thread) and
-// records the chunk's total; a second kernel adds the totals of the earlier
-// chunks of the row.
-constexpr int kScanChunk = 4096;
-
-
-__global__ __launch_bounds__(1024) void k_topk_scan_local(const uint32_t *__restrict__ tile_cnt,
-                                                          uint32_t *__restrict__ tile_off,
-                                                          uint32_t *__restrict__ chunk_sum, int64_t n_tiles,
-                                                          int64_t n_chunks) {
+// 8. Exclusive scan of the chunk totals of each row (one workgroup per row).
+__global__ __launch_bounds__(1024) void k_topk_chunk_scan(TopkRow *__restrict__ rows,
+                                                          const uint32_t *__restrict__ chunk_sum,
+                                                          uint32_t *__restrict__ chunk_off, int64_t n_chunks) {
     __shared__ uint32_t wsum[16];
-    const int m = blockIdx.y;
-    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kScanChunk + 4 * threadIdx.x;
-    const uint32_t *cr = tile_cnt + static_cast<int64_t>(m) * n_tiles;
-    uint32_t *orow = tile_off + static_cast<int64_t>(m) * n_tiles;
-    uint32_t c[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) c[j] = (t0 + j < n_tiles) ? cr[t0 + j] : 0u;
-    uint32_t total;
-    uint32_t run = block_exclusive_scan(c[0] + c[1] + c[2] + c[3], wsum, total);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        if (t0 + j < n_tiles) orow[t0 + j] = run;
-        run += c[j];
+    const int m = blockIdx.x;
+    const uint32_t *src = chunk_sum + static_cast<int64_t>(m) * n_chunks;
+    uint32_t *dst = chunk_off + static_cast<int64_t>(m) * n_chunks;
+    uint32_t carry = 0;
+    for (int64_t c0 = 0; c0 < n_chunks; c0 += 1024) {
+        const int64_t c = c0 + threadIdx.x;
+        const uint32_t v = c < n_chunks ? src[c] : 0u;
+        uint32_t total;
+        const uint32_t ex = block_exclusive_scan(v, wsum, total);
+        if (c < n_chunks) dst[c] = carry + ex;
+        carry += total;
+        __syncthreads();  // wsum is reused by the next round's scan
     }
-    if (threadIdx.x == 0) chunk_sum[static_cast<int64_t>(m) * n_chunks + blockIdx.x] = total;
-}
-
-__global__ __launch_bounds__(1024) void k_topk_scan_add(TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_off,
-                                                        const uint32_t *__restrict__ chunk_sum, int64_t n_tiles,
-                                                        int64_t n_chunks) {
-    __shared__ uint32_t base;
-    const int m = blockIdx.y;
-    const int64_t c = blockIdx.x;
-    if (threadIdx.x < 64) {
-        uint32_t s = 0;
-        for (int64_t j = threadIdx.x; j < c; j += 64) s += chunk_sum[static_cast<int64_t>(m) * n_chunks + j];
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-        if (threadIdx.x == 0) {
-            base = s;
-            if (c == n_chunks - 1) rows[m].total = s + chunk_sum[static_cast<int64_t>(m) * n_chunks + c];
-        }
-    }
-    __syncthreads();
-    const uint32_t b = base;
-    if (b == 0) return;
-    uint32_t *orow = tile_off + static_cast<int64_t>(m) * n_tiles;
-    const int64_t t0 = c * kScanChunk + 4 * threadIdx.x;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        if (t0 + j < n_tiles) orow[t0 + j] += b;
+    if (threadIdx.x == 0) rows[m].total = carry;
 }
 
 // Server side: scatter the messages to the dense p-hat (unpack); indices at
@@ -866,9 +1095,10 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
     TopkScratch &S = P.topk;
     const dqgan_desc &D = P.desc;
     S.n_tiles = D.ld / kTopkTile;
-    S.n_chunks = (D.d + kSampleStride - 1) / kSampleStride;
+    S.n_chunks = (S.n_tiles + kTopkChunkTiles - 1) / kTopkChunkTiles;
+    S.n_sample_chunks = (D.d + kSampleStride - 1) / kSampleStride;
     int64_t ns = 0;
-    for (int64_t c = 0; c < S.n_chunks; ++c) {
+    for (int64_t c = 0; c < S.n_sample_chunks; ++c) {
         const int64_t a = c * kSampleStride;
         ns += (D.d - a < kTopkTile) ? D.d - a : kTopkTile;
     }
@@ -876,20 +1106,31 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
     int64_t cap = D.k > 65536 ? D.k : 65536;
     S.cap = cap < D.d ? cap : D.d;
     const size_t M = static_cast<size_t>(D.M);
+    const size_t digit_words = M * kSelectPasses * kDigitBins;
     hipError_t e = hipMalloc(reinterpret_cast<void **>(&S.rows), M * sizeof(TopkRow));
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.hist), M * kSampleBins * sizeof(uint32_t));
+    // the sample histogram starts at zero; every iteration zeroes it again once read
+    if (e == hipSuccess) e = hipMemset(S.hist, 0, M * kSampleBins * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.sel_hist), M * kDigitBins * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.fb_hist), digit_words * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.cand), M * static_cast<size_t>(S.cap) * sizeof(uint2));
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.play), M * static_cast<size_t>(S.cap) * sizeof(uint2));
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.runs), M * static_cast<size_t>(S.n_chunks) * sizeof(uint2));
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.tile_cnt), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.tile_off), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
-    const int64_t nsc = (S.n_tiles + kScanChunk - 1) / kScanChunk;
     if (e == hipSuccess)
-        e = hipMalloc(reinterpret_cast<void **>(&S.chunk_sum), M * static_cast<size_t>(nsc) * sizeof(uint32_t));
+        e = hipMalloc(reinterpret_cast<void **>(&S.chunk_sum), M * static_cast<size_t>(S.n_chunks) * sizeof(uint32_t));
+    if (e == hipSuccess)
+        e = hipMalloc(reinterpret_cast<void **>(&S.chunk_off), M * static_cast<size_t>(S.n_chunks) * sizeof(uint32_t));
     S.n_agg_tiles = (D.ld + kAggTile - 1) / kAggTile;
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.agg_start),
                       M * static_cast<size_t>(S.n_agg_tiles + 1) * sizeof(uint32_t));
+    if (e == hipSuccess) e = hipDeviceSynchronize();  // the memset is done before the plan is used
     return e;
 }
 
@@ -897,10 +1138,15 @@ void topk_free(dqgan_plan_s &P) {
     TopkScratch &S = P.topk;
     (void)hipFree(S.rows);
     (void)hipFree(S.hist);
+    (void)hipFree(S.sel_hist);
+    (void)hipFree(S.fb_hist);
     (void)hipFree(S.cand);
+    (void)hipFree(S.play);
+    (void)hipFree(S.runs);
     (void)hipFree(S.tile_cnt);
     (void)hipFree(S.tile_off);
     (void)hipFree(S.chunk_sum);
+    (void)hipFree(S.chunk_off);
     (void)hipFree(S.agg_start);
     S = TopkScratch{};
 }
@@ -909,29 +1155,30 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     const TopkScratch &S = P.topk;
     const dqgan_desc &D = P.desc;
     const unsigned M = static_cast<unsigned>(D.M);
-    const int64_t nh = static_cast<int64_t>(D.M) * kSampleBins;
-    hipLaunchKernelGGL(k_fill_u32, dim3(grid_for(nh, 1024)), dim3(kBlock), 0, st, S.hist, nh, 0u);
-    const int64_t sb = (S.n_chunks + kSampleThreads / 64 - 1) / (kSampleThreads / 64);
-    hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < 32 ? sb : 32), M), dim3(kSampleThreads), 0, st,
-                       G, E, eta, D.d, D.ld, S.n_chunks, S.hist);
-    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.rows, S.n_samples, D.d, D.k);
-    const int64_t per_block = kPassTilesPerBlock;
-    hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>((S.n_tiles + per_block - 1) / per_block), M),
-                       dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap);
-    hipLaunchKernelGGL(k_topk_select, dim3(M), dim3(1024), 0, st, S.rows, S.cand, S.cap, D.k, S.hist);
-    hipLaunchKernelGGL(k_topk_count, dim3(64, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, S.tile_cnt, S.n_tiles);
-    for (int pass = 0; pass < 6; ++pass) {
-        hipLaunchKernelGGL(k_topk_fb_hist, dim3(kFbBlocks, M), dim3(kBlock), 0, st, pass, G, E, eta, D.d, D.ld, S.rows,
-                           S.hist);
-        hipLaunchKernelGGL(k_topk_fb_digit, dim3(M), dim3(64), 0, st, pass, S.rows, S.hist);
-    }
-    hipLaunchKernelGGL(k_topk_fb_recount, dim3(256, M), dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, S.rows,
-                       S.tile_cnt);
-    const int64_t nsc = (S.n_tiles + kScanChunk - 1) / kScanChunk;
-    hipLaunchKernelGGL(k_topk_scan_local, dim3(static_cast<unsigned>(nsc), M), dim3(1024), 0, st, S.tile_cnt,
-                       S.tile_off, S.chunk_sum, S.n_tiles, nsc);
-    hipLaunchKernelGGL(k_topk_scan_add, dim3(static_cast<unsigned>(nsc), M), dim3(1024), 0, st, S.rows, S.tile_off,
-                       S.chunk_sum, S.n_tiles, nsc);
+    const int64_t sb = (S.n_sample_chunks + kSampleThreads / 64 - 1) / (kSampleThreads / 64);
+    hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < kSampleBlocks ? sb : kSampleBlocks), M),
+                       dim3(kSampleThreads), 0, st,
+                       G, E, eta, D.d, D.ld, S.n_sample_chunks, S.hist);
+    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.sel_hist, S.rows, S.n_samples, D.d, D.k);
+    hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>(S.n_chunks), M), dim3(kBlock), 0, st, G, E, eta, D.d,
+                       D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap, S.runs, S.n_chunks);
+    hipLaunchKernelGGL(k_topk_sel_top, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, D.k,
+                       S.sel_hist);
+    hipLaunchKernelGGL(k_topk_sel_collect, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, D.k,
+                       S.sel_hist, S.play);
+    hipLaunchKernelGGL(k_topk_sel_finish, dim3(M), dim3(1024), 0, st, S.rows, S.cap, D.k, S.sel_hist, S.play,
+                       S.fb_hist);
+    for (int pass = 0; pass < kSelectPasses; ++pass)
+        hipLaunchKernelGGL(k_topk_fb_hist, dim3(kFbBlocks), dim3(kBlock), 0, st, pass, G, E, eta, D.d, D.ld, D.M, D.k,
+                           S.rows, S.fb_hist);
+    hipLaunchKernelGGL(k_topk_fb_recount, dim3(256), dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, D.M, D.k,
+                       S.rows, S.fb_hist, S.tile_cnt);
+    hipLaunchKernelGGL(k_topk_spill_count, dim3(kSpillBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap,
+                       S.tile_cnt, S.n_tiles);
+    hipLaunchKernelGGL(k_topk_count_scan, dim3(static_cast<unsigned>((S.n_chunks + 3) / 4), M), dim3(kBlock), 0, st,
+                       S.rows, S.cand,
+                       S.cap, S.runs, S.tile_cnt, S.tile_off, S.chunk_sum, S.n_tiles, S.n_chunks);
+    hipLaunchKernelGGL(k_topk_chunk_scan, dim3(M), dim3(1024), 0, st, S.rows, S.chunk_sum, S.chunk_off, S.n_chunks);
     return hipGetLastError();
 }
 
