@@ -79,7 +79,7 @@ struct TopkScratch {
     uint32_t *tile_off = nullptr;   // [M][n_tiles] selected elements before the tile within its chunk
     uint32_t *chunk_sum = nullptr;  // [M][n_chunks] selected elements per chunk of kTopkChunkTiles tiles
     uint32_t *chunk_off = nullptr;  // [M][n_chunks] exclusive prefix of chunk_sum
-    uint32_t *agg_start = nullptr;  // [M][n_agg_tiles + 1] first message entry per server-average tile
+    uint32_t *agg_start = nullptr;  // [n_agg_tiles + 1][M] first message entry per server-average tile
     int64_t n_agg_tiles = 0;
     int64_t n_tiles = 0;
     int64_t n_chunks = 0;           // chunks of kTopkChunkTiles tiles per row

@@ -916,170 +916,493 @@ __global__ __launch_bounds__(kBlock) void k_topk_scatter(const float *__restrict
     }
 }
 
-// Server average of the M top-k messages by column tiles.  Each worker's
-// list is sorted by index, so its entries in tile T are one run
-// [start(m, T), start(m, T+1)).  A workgroup stages the runs of all workers
-// in LDS; each thread then adds the entries of its own columns worker by
-// worker, so every column's sum is the ascending-worker sum from 0 the
-// definition gives; the tile is written once.  A tile with more entries
-// than the stage holds adds the runs from memory, worker by worker with a
-// barrier between workers.  Indices outside the tile (only a malformed
-// message has them) are skipped.
-constexpr int kAggTile = 2048;   // columns per workgroup
-constexpr int kAggStage = 2048;  // message entries staged per workgroup (32 KiB of LDS in all)
+// Server average of the M top-k messages by column tiles: the average of
+// the decoded messages, summed in ascending worker order in binary32.  Each
+// worker's list is sorted by index, so its entries in tile T are one run
+// [start(T, m), start(T + 1, m)).  Each thread of a workgroup owns kAggCols
+// columns of the tile (4 consecutive in each half) and carries their sums in
+// registers across the groups of 64 workers.  A group takes one of two
+// routes:
+//  - sparse (at most kAggStage entries): every run is staged in LDS and each
+//    staged entry sets its worker's bit in its column's 64-bit mask; a scan
+//    of the columns' entry counts places each entry at its column's first
+//    position plus the number of lower workers in the mask; each thread then
+//    adds its columns' entries in that order;
+//  - dense: rounds of kAggDenseRows workers.  A round's runs are read in
+//    aligned 16-byte chunks and scattered to one LDS row per worker (a
+//    column without an entry holds +0); each thread adds its columns of the
+//    rows in worker order, then clears them.  The next round's first chunks
+//    are loaded before the current round is summed.
+// The sums start from +0.  A partial sum started from +0 is never -0, so
+// adding the +0 of a worker without an entry changes nothing, and the sum
+// over the present entries equals the definition's sum over all M decoded
+// rows, except in one case: every worker sent -0 for the column, where the
+// definition gives -0.  That is the case exactly when the sum is +0 and
+// every one of the M terms has its sign bit set, which the unsigned minimum
+// of the terms' bit patterns (a worker without an entry counting as +0)
+// tells.  Indices outside the tile, and runs longer than the tile (only a
+// malformed message has them), are skipped and cut to the tile's width.
+constexpr int kAggTile = 2048;      // columns per tile
+constexpr int kAggHalf = kAggTile / 2;
+constexpr int kAggStage = 2048;     // entries of a group staged on the sparse route
+constexpr int kAggGroup = 64;       // workers per group: the bits of a column mask
+constexpr int kAggCols = kAggTile / kBlock;  // columns per thread
+constexpr int kAggDenseRows = 5;    // workers per round on the dense route
+constexpr int kAggDenseU = 3;       // 16-byte chunks per thread and load on the dense route
+constexpr int kAggStrip = 4;        // tiles per workgroup: tiles b, b + grid, ...
+static_assert(kAggCols == 8 && kAggHalf == 4 * kBlock, "each thread's columns are one float4 per half");
 
-// start(m, T) = the first entry j of worker m with idx[j] >= T * kAggTile,
-// for T = 0 .. n_t (k for the tiles past the last entry).  A wave takes
-// kStartsPer * 64 consecutive entries in coalesced rounds (round u: entry
-// u * 64 + lane), all loaded before the first is examined; the previous
-// entry's index comes from the neighbouring lane.
-constexpr int kStartsPer = 16;
+// column i (0..7) of thread t: 4t + i in the first half, 1024 + 4t + i - 4 in the second
+__device__ __forceinline__ int agg_col(int t, int i) { return (i < 4 ? 0 : kAggHalf - 4) + 4 * t + i; }
 
-__global__ __launch_bounds__(kBlock) void k_topk_agg_starts(const uint32_t *__restrict__ idx, int64_t k, int64_t n_t,
-                                                            uint32_t *__restrict__ start) {
+// start(T, m) = the first entry j of worker m with idx[j] >= T * kAggTile,
+// for T = 0 .. n_t (k for the tiles past the last entry), stored [T][M] so
+// that a tile's M starts are contiguous.  Entry j starts the tiles
+// (tile(j - 1), tile(j)] (tile(-1) = -1; entry k stands for the end, in
+// tile n_t).  The lists are read in aligned 16-byte chunks of the flat
+// [M][k] array: a wave takes kStartsLoads * 64 consecutive chunks of a row
+// in coalesced rounds (round u: chunk u * 64 + lane), all loaded before the
+// first is examined; a chunk's entries outside the row are not the row's.
+// A round whose last entry lies in the tile of the entry before the round
+// starts nothing (sorted lists) and is passed over.  Otherwise an entry that
+// starts one tile writes it; where one starts several (a run of empty
+// tiles) the wave writes them together, lane q taking the q-th.
+constexpr int kStartsLoads = 4;
+
+__device__ __forceinline__ uint32_t u4_at(const uint4 &v, int i) {
+    return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
+}
+
+__global__ __launch_bounds__(kBlock) void k_topk_agg_starts(const uint32_t *__restrict__ idx, int64_t k, int32_t M,
+                                                            int32_t n_t, uint32_t *__restrict__ start) {
     const int m = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const uint32_t *row = idx + static_cast<int64_t>(m) * k;
-    uint32_t *srow = start + static_cast<int64_t>(m) * (n_t + 1);
-    const int64_t jw = (static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave) * (64 * kStartsPer);
-    if (jw > k) return;
-    uint32_t v[kStartsPer];
+    const int64_t row0 = static_cast<int64_t>(m) * k;  // flat index of the row's first entry
+    const int64_t c_first = row0 >> 2;
+    const int64_t c_last = (row0 + k - 1) >> 2;               // the last chunk holding an entry of the row
+    const int64_t n_ch = ((row0 + k) >> 2) - c_first + 1;     // ... and the chunk of the end (entry k)
+    const int64_t cw = (static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave) * (64 * kStartsLoads);
+    if (cw >= n_ch) return;
+    const uint4 *chunks = reinterpret_cast<const uint4 *>(idx);
+    uint4 v[kStartsLoads];
 #pragma unroll
-    for (int u = 0; u < kStartsPer; ++u) {
-        const int64_t j = jw + 64 * u + lane;
-        v[u] = j < k ? row[j] : 0u;
+    for (int u = 0; u < kStartsLoads; ++u) {
+        const int64_t c = c_first + cw + 64 * u + lane;
+        v[u] = chunks[c < c_last ? c : c_last];
     }
-    const uint32_t before = jw > 0 ? row[jw - 1] : 0u;  // the entry before the wave's first
-    uint32_t last_prev_round = before;
+    // the tile of an entry: -1 before the row, n_t for the end and past it
+    auto tile_of = [&](int64_t j, uint32_t x) -> int {
+        return j < 0 ? -1 : j < k ? min(static_cast<int>(x / kAggTile), n_t) : n_t;
+    };
+    const int64_t j_wave = 4 * (c_first + cw) - row0;  // the wave's first entry (row-relative)
+    int t_before = j_wave - 1 >= 0 ? tile_of(j_wave - 1, idx[row0 + j_wave - 1]) : -1;
 #pragma unroll
-    for (int u = 0; u < kStartsPer; ++u) {
-        const int64_t j = jw + 64 * u + lane;
-        const uint32_t up = __shfl_up(v[u], 1);
-        const uint32_t prev_idx = lane > 0 ? up : last_prev_round;
-        last_prev_round = __shfl(v[u], 63);
-        if (j > k) continue;
-        const int64_t tj = j < k ? min(static_cast<int64_t>(v[u] / kAggTile), n_t) : n_t;
-        const int64_t tp = j > 0 ? min(static_cast<int64_t>(prev_idx / kAggTile), n_t) : -1;
-        for (int64_t T = tp + 1; T <= tj; ++T) srow[T] = static_cast<uint32_t>(j);
+    for (int u = 0; u < kStartsLoads; ++u) {
+        const int64_t j0 = j_wave + 4 * (64 * u + lane);  // row-relative index of the chunk's entry 0
+        int t[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) t[i] = tile_of(j0 + i, u4_at(v[u], i));
+        const int t_round_last = __builtin_amdgcn_readlane(t[3], 63);
+        if (t_round_last == t_before) continue;  // no entry of the round starts a tile
+        const int t_prev_lane = __shfl_up(t[3], 1);
+        int n[4];
+        int tp = lane > 0 ? t_prev_lane : t_before;
+        bool many = false;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            n[i] = t[i] > tp ? t[i] - tp : 0;
+            many = many || n[i] > 1;
+            tp = t[i] > tp ? t[i] : tp;
+        }
+        t_before = t_round_last;
+        if (__ballot(many) == 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (n[i] == 1) start[static_cast<int64_t>(t[i]) * M + m] = static_cast<uint32_t>(j0 + i);
+            continue;
+        }
+        // some entry starts several tiles: entry i of every lane in turn,
+        // the wave writing their starts together
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t ni = static_cast<uint32_t>(n[i]);
+            uint32_t incl = ni;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const uint32_t x = __shfl_up(incl, o);
+                if (lane >= o) incl += x;
+            }
+            const uint32_t total = __shfl(incl, 63);
+            for (uint32_t q0 = 0; q0 < total; q0 += 64) {
+                const uint32_t q = q0 + lane;
+                int o = 0;  // the owner of start q: the number of lanes with incl <= q
+#pragma unroll
+                for (int sh = 32; sh > 0; sh >>= 1)
+                    if (static_cast<uint32_t>(__shfl(incl, o + sh - 1)) <= q) o += sh;
+                const uint32_t o_incl = __shfl(incl, o);
+                const int o_t = __shfl(t[i], o);
+                if (q < total) {
+                    const int64_t T = static_cast<int64_t>(o_t) - (o_incl - 1 - q);  // o's tiles end at o_t
+                    const int64_t j = j_wave + 4 * (64 * u + o) + i;
+                    start[T * M + m] = static_cast<uint32_t>(j);
+                }
+            }
+        }
     }
 }
 
-static_assert(kAggTile % kBlock == 0, "each thread owns the same number of columns of a tile");
-constexpr int kAggMaxM = 1024;            // the library's largest worker count
-constexpr int kAggPerThread = kAggMaxM / kBlock;  // workers per thread in the run scan
+// A barrier that orders LDS only: outstanding global loads stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+union AggLds {
+    struct {
+        unsigned long long mask[kAggTile];  // bit w: worker g0 + w has an entry in the column
+        uint16_t col_base[kAggTile];        // first position of the column's entries in `placed`
+        uint16_t st_col[kAggStage];         // staged entries: column (0xFFFF: outside the tile),
+        uint8_t st_w[kAggStage];            //   worker within the group,
+        float st_val[kAggStage];            //   value
+        float placed[kAggStage];            // the values in (column, worker) order
+    } s;
+    float rows[kAggDenseRows][kAggTile];    // dense route: one row per worker of a round
+};
+
+// A group's runs as the dense route reads them: worker w's run starts at
+// entry G0 = (g0 + w) * k + start of the flat [M][k] lists; its chunks are
+// the 16-byte words c0 .. c0 + nc - 1 with c0 = G0 / 4, and the run's first
+// entry is entry lo = G0 % 4 of chunk c0.  ch_off is the exclusive prefix of
+// the chunk counts over the group.
+struct AggRuns {
+    uint32_t run_s[kAggGroup], woff[kAggGroup + 1];
+    unsigned long long ch_c0[kAggGroup];
+    uint32_t ch_off[kAggGroup + 1];
+    uint32_t ch_lo[kAggGroup];
+};
+
+// Chunks of one load of the dense route: chunk q0 + tid + kBlock * u of the
+// round's workers w0 .. w1 - 1 (their chunks ch_off[w0] .. ch_off[w1]),
+// with a 4-bit mask of the entries that belong to the run and the row.
+struct DenseChunks {
+    uint4 idx[kAggDenseU];
+    f32x4 val[kAggDenseU];
+    uint32_t tag[kAggDenseU];  // bits 0..3: entries of the run; bits 4..: row of the round
+};
+
+__device__ __forceinline__ void agg_dense_load(DenseChunks &L, const float *__restrict__ val,
+                                               const uint32_t *__restrict__ idx, const AggRuns &R, int w0, int w1,
+                                               uint32_t q0) {
+    const uint32_t a = R.ch_off[w0], e = R.ch_off[w1];
+    const uint32_t o1 = R.ch_off[w0 + 1 < w1 ? w0 + 1 : w1], o2 = R.ch_off[w0 + 2 < w1 ? w0 + 2 : w1],
+                   o3 = R.ch_off[w0 + 3 < w1 ? w0 + 3 : w1], o4 = R.ch_off[w0 + 4 < w1 ? w0 + 4 : w1];
+    static_assert(kAggDenseRows == 5, "the row search below covers five rows");
+#pragma unroll
+    for (int u = 0; u < kAggDenseU; ++u) {
+        const uint32_t Q0 = a + q0 + threadIdx.x + kBlock * u;
+        const bool live = Q0 < e;
+        const uint32_t Q = live ? Q0 : a;  // past the end: the round's first chunk, masked out
+        const int r = (Q >= o1) + (Q >= o2) + (Q >= o3) + (Q >= o4);
+        const int w = w0 + r;
+        const uint32_t ql = Q - R.ch_off[w];
+        const unsigned long long c = R.ch_c0[w] + ql;
+        L.idx[u] = reinterpret_cast<const uint4 *>(idx)[c];
+        L.val[u] = reinterpret_cast<const f32x4 *>(val)[c];
+        const int rel = static_cast<int>(4 * ql) - static_cast<int>(R.ch_lo[w]);
+        const int n = static_cast<int>(R.woff[w + 1] - R.woff[w]);
+        uint32_t m4 = 0u;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m4 |= (live && rel + i >= 0 && rel + i < n) ? (1u << i) : 0u;
+        L.tag[u] = m4 | (static_cast<uint32_t>(r) << 4);
+    }
+}
+
+__device__ __forceinline__ void agg_dense_scatter(const DenseChunks &L, AggLds &S, uint32_t base_lo, bool addressable) {
+#pragma unroll
+    for (int u = 0; u < kAggDenseU; ++u) {
+        float *row = S.rows[L.tag[u] >> 4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t c = (i == 0 ? L.idx[u].x : i == 1 ? L.idx[u].y : i == 2 ? L.idx[u].z : L.idx[u].w) - base_lo;
+            if (((L.tag[u] >> i) & 1u) && addressable && c < static_cast<uint32_t>(kAggTile)) row[c] = elem(L.val[u], i);
+        }
+    }
+}
+
+// Chunks of one load of the sparse route: chunk q0 + tid + kBlock * u of
+// the whole group (chunks 0 .. ch_off[gn]), with the stage position of the
+// chunk's entry 0 and a 4-bit mask of the entries that belong to the run.
+struct SparseChunks {
+    uint4 idx[kAggDenseU];
+    f32x4 val[kAggDenseU];
+    int pos[kAggDenseU];       // stage position of entry 0 (entries 1..3 follow)
+    uint32_t tag[kAggDenseU];  // bits 0..3: entries of the run; bits 4..: worker in the group
+};
+
+__device__ __forceinline__ void agg_sparse_load(SparseChunks &L, const float *__restrict__ val,
+                                                const uint32_t *__restrict__ idx, const AggRuns &R, int gn,
+                                                uint32_t q0) {
+    const uint32_t e = R.ch_off[gn];
+#pragma unroll
+    for (int u = 0; u < kAggDenseU; ++u) {
+        const uint32_t Q0 = q0 + threadIdx.x + kBlock * u;
+        const bool live = Q0 < e;
+        const uint32_t Q = live ? Q0 : 0u;  // past the end: the group's first chunk, masked out
+        int lo = 0, hi = gn - 1;            // the last worker whose first chunk is <= Q
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (R.ch_off[mid] <= Q) lo = mid;
+            else hi = mid - 1;
+        }
+        const uint32_t ql = Q - R.ch_off[lo];
+        const unsigned long long c = R.ch_c0[lo] + ql;
+        L.idx[u] = reinterpret_cast<const uint4 *>(idx)[c];
+        L.val[u] = reinterpret_cast<const f32x4 *>(val)[c];
+        const int rel = static_cast<int>(4 * ql) - static_cast<int>(R.ch_lo[lo]);
+        const int n = static_cast<int>(R.woff[lo + 1] - R.woff[lo]);
+        uint32_t m4 = 0u;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m4 |= (live && rel + i >= 0 && rel + i < n) ? (1u << i) : 0u;
+        L.pos[u] = static_cast<int>(R.woff[lo]) + rel;
+        L.tag[u] = m4 | (static_cast<uint32_t>(lo) << 4);
+    }
+}
 
 __global__ __launch_bounds__(kBlock) void k_topk_agg_tiles(const float *__restrict__ val,
                                                            const uint32_t *__restrict__ idx, int64_t k, int32_t M,
                                                            const uint32_t *__restrict__ start, int64_t n_t,
                                                            int64_t d, int64_t ld, float *__restrict__ Qhat,
                                                            float invM) {
-    __shared__ float acc[kAggTile];
-    __shared__ uint32_t st_col[kAggStage];
-    __shared__ float st_val[kAggStage];
-    __shared__ uint32_t run_s[kAggMaxM];     // first entry of each worker's run
-    __shared__ uint32_t woff[kAggMaxM + 1];  // staged offset of each worker's run
+    __shared__ AggLds S;
+    __shared__ AggRuns R;
     __shared__ uint32_t wsum[kBlock / 64];
-    const int64_t T = blockIdx.x;
-    const int64_t base = T * kAggTile;
     const int tid = threadIdx.x;
-    for (int c = tid; c < kAggTile; c += kBlock) acc[c] = 0.0f;
-    // runs of workers kAggPerThread*tid ...: clamped to [0, k]
-    uint32_t rs[kAggPerThread], rn[kAggPerThread], mine = 0;
-#pragma unroll
-    for (int u = 0; u < kAggPerThread; ++u) {
-        const int m = kAggPerThread * tid + u;
-        rs[u] = 0u;
-        rn[u] = 0u;
-        if (m < M) {
-            const uint32_t *srow = start + static_cast<int64_t>(m) * (n_t + 1);
-            const int64_t s = min(static_cast<int64_t>(srow[T]), k);
-            const int64_t e = min(static_cast<int64_t>(srow[T + 1]), k);
-            rs[u] = static_cast<uint32_t>(s);
-            rn[u] = e > s ? static_cast<uint32_t>(e - s) : 0u;
-        }
-        mine += rn[u];
-    }
-    // exclusive scan of the per-thread counts over the workgroup
     const int lane = tid & 63, wave = tid >> 6;
-    uint32_t incl = mine;
+    const int n_groups = (M + kAggGroup - 1) / kAggGroup;
+    const int n_it = kAggStrip * n_groups;  // (tile, group) pairs of this workgroup
+    // Every wave reads the starts itself, so that each knows a tile's entry
+    // count without LDS; with one group they are read for the whole strip
+    // up front.
+    uint32_t ss[kAggStrip], ee[kAggStrip];
+    if (n_groups == 1) {
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t x = __shfl_up(incl, o);
-        if (lane >= o) incl += x;
+        for (int q = 0; q < kAggStrip; ++q) {
+            const int64_t T = blockIdx.x + static_cast<int64_t>(q) * gridDim.x;
+            ss[q] = ee[q] = 0u;
+            if (T < n_t && lane < M) {
+                ss[q] = start[T * M + lane];
+                ee[q] = start[(T + 1) * M + lane];
+            }
+        }
     }
-    if (lane == 63) wsum[wave] = incl;
-    __syncthreads();
-    uint32_t o = incl - mine, total = 0;
-    for (int w = 0; w < kBlock / 64; ++w) {
-        if (w < wave) o += wsum[w];
-        total += wsum[w];
-    }
+    float acc[kAggCols];
+    uint32_t mn[kAggCols];  // unsigned minimum of the terms' bit patterns
+    for (int it = 0; it < n_it; ++it) {
+        const int sq = it / n_groups;
+        const int64_t T = blockIdx.x + static_cast<int64_t>(sq) * gridDim.x;
+        if (T >= n_t) break;  // uniform: the strip's later tiles are past the end too
+        const int g0 = (it % n_groups) * kAggGroup;
+        const int gn = M - g0 < kAggGroup ? M - g0 : kAggGroup;
+        const int64_t base = T * kAggTile;
+        if (g0 == 0) {
 #pragma unroll
-    for (int u = 0; u < kAggPerThread; ++u) {
-        const int m = kAggPerThread * tid + u;
-        if (m < M) {
-            run_s[m] = rs[u];
-            woff[m] = o;
-        }
-        o += rn[u];
-    }
-    if (tid == 0) woff[M] = total;
-    __syncthreads();
-    if (total <= kAggStage) {
-        // stage every run: staged entry g belongs to the last worker whose
-        // offset is <= g (binary search over the offsets)
-        for (uint32_t g = tid; g < total; g += kBlock) {
-            int lo = 0, hi = M - 1;
-            while (lo < hi) {
-                const int mid = (lo + hi + 1) >> 1;
-                if (woff[mid] <= g) lo = mid;
-                else hi = mid - 1;
-            }
-            const int64_t j = static_cast<int64_t>(run_s[lo]) + (g - woff[lo]);
-            st_col[g] = idx[static_cast<int64_t>(lo) * k + j];
-            st_val[g] = val[static_cast<int64_t>(lo) * k + j];
-        }
-        __syncthreads();
-        // Thread tid owns columns [8 tid, 8 tid + 8) of the tile and adds
-        // their entries worker by worker in ascending order: a binary search
-        // finds each worker's first entry at or beyond the thread's first
-        // column, and the worker's run is sorted, so no barrier is needed.
-        const int64_t c0 = static_cast<int64_t>(kAggTile / kBlock) * tid;
-        for (int m = 0; m < M; ++m) {
-            uint32_t lo = woff[m], hi = woff[m + 1];
-            const uint32_t end = hi;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi) >> 1;
-                if (static_cast<int64_t>(st_col[mid]) < base + c0) lo = mid + 1;
-                else hi = mid;
-            }
-            for (uint32_t j = lo; j < end; ++j) {
-                const int64_t c = static_cast<int64_t>(st_col[j]) - base - c0;
-                if (c >= kAggTile / kBlock) break;
-                if (c >= 0) acc[c0 + c] = add_rn(acc[c0 + c], st_val[j]);
+            for (int i = 0; i < kAggCols; ++i) {
+                acc[i] = 0.0f;
+                mn[i] = 0xFFFFFFFFu;
             }
         }
-        __syncthreads();
-    } else {
-        // a dense tile: the runs straight from memory, worker by worker
-        for (int m = 0; m < M; ++m) {
-            const int64_t s = run_s[m], n = woff[m + 1] - woff[m];
-            const float *vrow = val + static_cast<int64_t>(m) * k;
-            const uint32_t *irow = idx + static_cast<int64_t>(m) * k;
-            for (int64_t j = tid; j < n; j += kBlock) {
-                const int64_t c = static_cast<int64_t>(irow[s + j]) - base;
-                if (c >= 0 && c < kAggTile) acc[c] = add_rn(acc[c], vrow[s + j]);
-            }
-            __syncthreads();
+        uint32_t s_raw = 0u, e_raw = 0u;
+        if (n_groups == 1) {
+#pragma unroll
+            for (int q = 0; q < kAggStrip; ++q)
+                if (q == sq) {
+                    s_raw = ss[q];
+                    e_raw = ee[q];
+                }
+        } else if (lane < gn) {
+            s_raw = start[T * M + g0 + lane];
+            e_raw = start[(T + 1) * M + g0 + lane];
         }
-    }
-    for (int c = tid; c < kAggTile; c += kBlock) {
-        const int64_t i = base + c;
-        if (i >= ld) break;
-        const float sacc = acc[c];
-        Qhat[i] = i >= d ? 0.0f
-                         : invM > 0.0f ? mul_rn(sacc, invM)
-                                       : static_cast<float>(static_cast<double>(sacc) / static_cast<double>(M));
+        const int64_t s0 = min(static_cast<int64_t>(s_raw), k);
+        const int64_t e0 = min(static_cast<int64_t>(e_raw), k);
+        const uint32_t rn = e0 > s0 ? static_cast<uint32_t>(min(e0 - s0, static_cast<int64_t>(kAggTile))) : 0u;
+        uint32_t incl = rn;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t x = __shfl_up(incl, o);
+            if (lane >= o) incl += x;
+        }
+        const uint32_t total = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(incl), 63));
+        if (total == 0u) {
+#pragma unroll
+            for (int i = 0; i < kAggCols; ++i) mn[i] = 0u;  // every term is +0
+        } else {
+            // the group's runs, their offsets and chunks, for every wave (wave 0 writes them)
+            if (wave == 0) {
+                const unsigned long long G0 = static_cast<unsigned long long>(g0 + lane) * static_cast<unsigned long long>(k) +
+                                              static_cast<unsigned long long>(s0);
+                const unsigned long long c0 = G0 >> 2;
+                const uint32_t nc = rn ? static_cast<uint32_t>(((G0 + rn + 3) >> 2) - c0) : 0u;
+                uint32_t cincl = nc;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const uint32_t y = __shfl_up(cincl, o);
+                    if (lane >= o) cincl += y;
+                }
+                R.run_s[lane] = static_cast<uint32_t>(s0);
+                R.woff[lane] = incl - rn;
+                R.ch_c0[lane] = c0;
+                R.ch_off[lane] = cincl - nc;
+                R.ch_lo[lane] = static_cast<uint32_t>(G0 & 3u);
+                if (lane == 63) {
+                    R.woff[kAggGroup] = incl;
+                    R.ch_off[kAggGroup] = cincl;
+                }
+            }
+            lds_barrier();
+            if (total <= kAggStage) {
+                for (int c = tid; c < kAggTile; c += kBlock) S.s.mask[c] = 0ull;
+                lds_barrier();
+                // stage every run and mark each entry's worker in its column
+                const uint32_t base_lo = static_cast<uint32_t>(base);
+                const bool addressable = (static_cast<unsigned long long>(base) >> 32) == 0;  // idx is 32-bit
+                for (uint32_t q0 = 0; q0 < R.ch_off[gn]; q0 += kBlock * kAggDenseU) {
+                    SparseChunks L;
+                    agg_sparse_load(L, val, idx, R, gn, q0);
+#pragma unroll
+                    for (int u = 0; u < kAggDenseU; ++u) {
+                        const uint32_t w = L.tag[u] >> 4;
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            if (!((L.tag[u] >> i) & 1u)) continue;
+                            const uint32_t c = u4_at(L.idx[u], i) - base_lo;
+                            const bool in = addressable && c < static_cast<uint32_t>(kAggTile);
+                            const int g = L.pos[u] + i;
+                            S.s.st_col[g] = in ? static_cast<uint16_t>(c) : static_cast<uint16_t>(0xFFFFu);
+                            S.s.st_w[g] = static_cast<uint8_t>(w);
+                            S.s.st_val[g] = elem(L.val[u], i);
+                            if (in) atomicOr(&S.s.mask[c], 1ull << w);
+                        }
+                    }
+                }
+                lds_barrier();
+                // each column's first position: exclusive scan of the entry counts
+                uint32_t cnt[kAggCols], mine = 0u;
+#pragma unroll
+                for (int i = 0; i < kAggCols; ++i) {
+                    cnt[i] = static_cast<uint32_t>(__popcll(S.s.mask[agg_col(tid, i)]));
+                    mine += cnt[i];
+                }
+                uint32_t incl = mine;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const uint32_t x = __shfl_up(incl, o);
+                    if (lane >= o) incl += x;
+                }
+                if (lane == 63) wsum[wave] = incl;
+                lds_barrier();
+                uint32_t pos = incl - mine;
+                for (int w = 0; w < wave; ++w) pos += wsum[w];
+#pragma unroll
+                for (int i = 0; i < kAggCols; ++i) {
+                    S.s.col_base[agg_col(tid, i)] = static_cast<uint16_t>(pos);
+                    pos += cnt[i];
+                }
+                lds_barrier();
+                // each entry to its place: the column's first position plus the
+                // number of lower workers with an entry in the column
+                for (uint32_t g = tid; g < total; g += kBlock) {
+                    const uint32_t c = S.s.st_col[g];
+                    if (c == 0xFFFFu) continue;
+                    const unsigned long long below = (1ull << S.s.st_w[g]) - 1ull;
+                    S.s.placed[S.s.col_base[c] + __popcll(S.s.mask[c] & below)] = S.s.st_val[g];
+                }
+                lds_barrier();
+                // the columns' sums in ascending worker order
+#pragma unroll
+                for (int i = 0; i < kAggCols; ++i) {
+                    const uint32_t b = S.s.col_base[agg_col(tid, i)];
+                    uint32_t m = cnt[i] == static_cast<uint32_t>(gn) ? mn[i] : 0u;  // an absent worker: +0
+                    for (uint32_t q = 0; q < cnt[i]; ++q) {
+                        const float x = S.s.placed[b + q];
+                        acc[i] = add_rn(acc[i], x);
+                        m = min(m, __float_as_uint(x));
+                    }
+                    mn[i] = m;
+                }
+            } else {
+                // the rows start cleared; each thread clears its own columns
+                const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+                for (int r = 0; r < kAggDenseRows; ++r) {
+                    st4(&S.rows[r][4 * tid], zero);
+                    st4(&S.rows[r][kAggHalf + 4 * tid], zero);
+                }
+                const uint32_t base_lo = static_cast<uint32_t>(base);
+                const bool addressable = (static_cast<unsigned long long>(base) >> 32) == 0;  // idx is 32-bit
+                const int n_rounds = (gn + kAggDenseRows - 1) / kAggDenseRows;
+                DenseChunks L;
+                auto load = [&](int w0, uint32_t q0) {
+                    const int w1 = w0 + kAggDenseRows < gn ? w0 + kAggDenseRows : gn;
+                    if (R.ch_off[w1] - R.ch_off[w0] > q0) {
+                        agg_dense_load(L, val, idx, R, w0, w1, q0);
+                    } else {
+#pragma unroll
+                        for (int u = 0; u < kAggDenseU; ++u) L.tag[u] = 0u;
+                    }
+                };
+                load(0, 0u);
+                lds_barrier();  // the rows are cleared before the first scatter
+                for (int r = 0; r < n_rounds; ++r) {
+                    const int w0 = r * kAggDenseRows;
+                    const int w1 = w0 + kAggDenseRows < gn ? w0 + kAggDenseRows : gn;
+                    const uint32_t nch = R.ch_off[w1] - R.ch_off[w0];
+                    agg_dense_scatter(L, S, base_lo, addressable);
+                    for (uint32_t q0 = kBlock * kAggDenseU; q0 < nch; q0 += kBlock * kAggDenseU) {
+                        load(w0, q0);
+                        agg_dense_scatter(L, S, base_lo, addressable);
+                    }
+                    if (r + 1 < n_rounds) load(w1, 0u);
+                    lds_barrier();
+                    for (int rr = 0; rr < w1 - w0; ++rr) {
+                        const f32x4 x0 = ld4(&S.rows[rr][4 * tid]), x1 = ld4(&S.rows[rr][kAggHalf + 4 * tid]);
+#pragma unroll
+                        for (int c = 0; c < 4; ++c) {
+                            acc[c] = add_rn(acc[c], elem(x0, c));
+                            acc[c + 4] = add_rn(acc[c + 4], elem(x1, c));
+                            mn[c] = min(mn[c], __float_as_uint(elem(x0, c)));
+                            mn[c + 4] = min(mn[c + 4], __float_as_uint(elem(x1, c)));
+                        }
+                        st4(&S.rows[rr][4 * tid], zero);
+                        st4(&S.rows[rr][kAggHalf + 4 * tid], zero);
+                    }
+                    lds_barrier();
+                }
+            }
+            lds_barrier();  // the next pair rewrites the group's tables and the LDS buffers
+        }
+        if (g0 + gn == M) {
+            // ld is a multiple of 1024: a half's four columns are all inside or all outside
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int64_t col = base + h * kAggHalf + 4 * tid;
+                if (col < ld) {
+                    f32x4 q;
+#pragma unroll
+                    for (int c = 0; c < 4; ++c) {
+                        const int i = 4 * h + c;
+                        const bool neg0 = __float_as_uint(acc[i]) == 0u && mn[i] >= 0x80000000u;
+                        const float sacc = neg0 ? -0.0f : acc[i];
+                        set_elem(q, c, col + c >= d ? 0.0f
+                                       : invM > 0.0f ? mul_rn(sacc, invM)
+                                                     : static_cast<float>(static_cast<double>(sacc) /
+                                                                          static_cast<double>(M)));
+                    }
+                    st4(Qhat + col, q);
+                }
+            }
+        }
     }
 }
 
@@ -1201,13 +1524,15 @@ hipError_t launch_topk_unpack(const dqgan_plan_s &P, const dqgan_wire &w, float 
 hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, float *Qhat, hipStream_t st) {
     const dqgan_desc &D = P.desc;
     const TopkScratch &S = P.topk;
-    const int64_t per_block = static_cast<int64_t>(kBlock) * kStartsPer;
-    const int64_t sb = (D.k + 1 + per_block - 1) / per_block;
+    // a row spans at most k / 4 + 2 chunks, its end included
+    const int64_t per_block = static_cast<int64_t>(kBlock) * kStartsLoads;
+    const int64_t sb = (D.k / 4 + 2 + per_block - 1) / per_block;
     hipLaunchKernelGGL(k_topk_agg_starts, dim3(static_cast<unsigned>(sb), static_cast<unsigned>(D.M)), dim3(kBlock), 0,
-                       st, w.idx, D.k, S.n_agg_tiles, S.agg_start);
+                       st, w.idx, D.k, D.M, static_cast<int32_t>(S.n_agg_tiles), S.agg_start);
     const float im = (D.M & (D.M - 1)) == 0 ? 1.0f / static_cast<float>(D.M) : 0.0f;
-    hipLaunchKernelGGL(k_topk_agg_tiles, dim3(static_cast<unsigned>(S.n_agg_tiles)), dim3(kBlock), 0, st, w.val, w.idx,
-                       D.k, D.M, S.agg_start, S.n_agg_tiles, D.d, D.ld, Qhat, im);
+    const int64_t nb = (S.n_agg_tiles + kAggStrip - 1) / kAggStrip;
+    hipLaunchKernelGGL(k_topk_agg_tiles, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, st, w.val, w.idx, D.k, D.M,
+                       S.agg_start, S.n_agg_tiles, D.d, D.ld, Qhat, im);
     return hipGetLastError();
 }
 
