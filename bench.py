@@ -319,6 +319,49 @@ def measure(w, steps, warmup, graph_mode=False, copy_calibration=False, extras=T
     return out
 
 
+ALLOC_PADS_MIB = [0, 1, 3, 64, 130, 0, 2, 7, 513, 5]
+
+
+def alloc_trials(w, n, steps):
+    """Allocate the workload's buffers n times in this process (a padding
+    allocation of a few MiB before each, freed and returned to the driver
+    after each trial) and time `steps` iterations of each allocation.  The
+    same kernels on the same sizes run at different speeds depending on the
+    physical memory behind the buffers; this shows the spread.  One JSON line
+    per trial: the apply pass and the step in ms."""
+    import torch
+    import synth
+    from paper_2010_13359_amd import dqgan
+    dev = torch.device("cuda:0")
+    for trial in range(n):
+        pad_mib = ALLOC_PADS_MIB[trial % len(ALLOC_PADS_MIB)]
+        pad = torch.empty(pad_mib * 2 ** 18 + 1, device=dev) if pad_mib else None
+        plan = dqgan.Plan.from_workload(w)
+        G = synth.gradients(w, 1, device=dev)
+        E = torch.zeros((w.M, w.ld), dtype=torch.float32, device=dev)
+        W = synth.init_params(w, device=dev)
+        WX = torch.empty((w.M, w.ld), dtype=torch.float32, device=dev)
+        wire = plan.new_wire(dev)
+        apply_ms, step_ms = [], []
+        for t in range(steps + 1):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+            ev[0].record()
+            dqgan.step_scales(plan, w.eta, G, E, wire)
+            ev[1].record()
+            dqgan.step_apply(plan, w.eta, t + 1, G, E, W, WX, wire)
+            ev[2].record()
+            torch.cuda.synchronize()
+            if t > 0:  # the first iteration of each allocation is a warmup
+                apply_ms.append(ev[1].elapsed_time(ev[2]))
+                step_ms.append(ev[0].elapsed_time(ev[2]))
+        print(json.dumps({"trial": trial, "workload": workload_label(w), "pad_mib": pad_mib,
+                          "apply_ms": round(sum(apply_ms) / len(apply_ms), 3),
+                          "step_ms": round(sum(step_ms) / len(step_ms), 3)}), flush=True)
+        del G, E, W, WX, wire, pad
+        plan.close()
+        torch.cuda.empty_cache()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -334,6 +377,9 @@ def main():
     ap.add_argument("--graph", action="store_true",
                     help="capture the timed iterations in one HIP graph and time its replay (launch-bound sizes); "
                          "the per-pass times then come from an eager run of the same iterations")
+    ap.add_argument("--alloc-trials", type=int, default=0, metavar="N",
+                    help="instead of the bench line: allocate the workload N times in one process and print "
+                         "the apply-pass and step time of each allocation (one JSON line each)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: the library runs on one GPU; --gpus %d is not offered (the M workers are the rows of "
@@ -345,6 +391,9 @@ def main():
 
     torch.cuda.set_device(torch.device("cuda:0"))
     w = synth.get(args.config)
+    if args.alloc_trials:
+        alloc_trials(w, args.alloc_trials, max(1, min(args.steps, 5)))
+        return
     rec = measure(w, args.steps, args.warmup, args.graph, args.copy_calibration)
     out = {"metric": METRIC, "value": rec.pop("value"), "unit": rec.pop("unit"), "n_gpus": 1,
            "steps": rec.pop("steps"), "warmup": rec.pop("warmup"), "ms_per_step": rec.pop("ms_per_step"),

@@ -2,7 +2,8 @@
 dispatch count and duration statistics, and for counter runs the mean value of
 each counter per dispatch.
 
-    python -m paper_2010_13359_amd.rocprof_summary RESULTS.db [--skip-first N | --counters | --dispatches NAME]
+    python -m paper_2010_13359_amd.rocprof_summary RESULTS.db [--skip-first N | --counters | --dispatches NAME |
+                                                              --per-trial KERNEL GROUP]
 """
 import argparse
 import re
@@ -80,6 +81,32 @@ def counter_dispatches(db, match):
     return [dict(v, dispatch=k) for k, v in sorted(per.items())]
 
 
+def per_trial(db, match, group):
+    """Dispatches of the kernel whose short name equals `match`, in launch
+    order, taken in consecutive groups of `group` (one group per allocation
+    trial of bench.py --alloc-trials); per group, leaving out its first
+    dispatch (the warmup): mean duration and mean of each counter."""
+    con = sqlite3.connect(db)
+    disp = [(d, float(u)) for n, u, d in con.execute("select name, duration, dispatch_id from kernels order by start")
+            if short_name(n) == match]
+    ctr = {}
+    for name, c, d, v in con.execute("select kernel_name, counter_name, dispatch_id, value from counters_collection"):
+        if short_name(name) == match:
+            ctr.setdefault(d, {}).setdefault(c, 0.0)
+            ctr[d][c] += float(v)
+    out = []
+    for t in range(len(disp) // group):
+        grp = disp[group * t + 1: group * (t + 1)]
+        if not grp:
+            continue
+        rec = {"trial": t, "us": sum(u for _, u in grp) / len(grp) / 1e3}
+        names = sorted(ctr.get(grp[0][0], {}))
+        for c in names:
+            rec[c] = sum(ctr[d][c] for d, _ in grp) / len(grp)
+        out.append(rec)
+    return out
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     ap.add_argument("db")
@@ -87,7 +114,14 @@ def main(argv=None):
     ap.add_argument("--dispatches", metavar="NAME", help="per-dispatch counters of kernels whose name contains NAME")
     ap.add_argument("--skip-first", type=int, default=0, metavar="N",
                     help="leave out the first N dispatches of each kernel (warmup) from the duration statistics")
+    ap.add_argument("--per-trial", nargs=2, metavar=("KERNEL", "GROUP"),
+                    help="mean duration and counters of KERNEL per consecutive group of GROUP dispatches")
     a = ap.parse_args(argv)
+    if a.per_trial:
+        for rec in per_trial(a.db, a.per_trial[0], int(a.per_trial[1])):
+            print("trial %-3d %10.1f us  %s" % (rec.pop("trial"), rec.pop("us"),
+                                                "  ".join("%s=%.1f" % kv for kv in rec.items())))
+        return 0
     if a.dispatches:
         for d in counter_dispatches(a.db, a.dispatches):
             vals = "  ".join("%s=%.1f" % (k, v) for k, v in d.items() if k not in ("kernel", "grid", "dispatch"))
