@@ -944,11 +944,11 @@ __global__ __launch_bounds__(kBlock) void k_topk_scatter(const float *__restrict
 // malformed message has them), are skipped and cut to the tile's width.
 constexpr int kAggTile = 2048;      // columns per tile
 constexpr int kAggHalf = kAggTile / 2;
-constexpr int kAggStage = 2048;     // entries of a group staged on the sparse route
+constexpr int kAggStage = 1536;     // entries of a group staged on the sparse route
 constexpr int kAggGroup = 64;       // workers per group: the bits of a column mask
 constexpr int kAggCols = kAggTile / kBlock;  // columns per thread
-constexpr int kAggDenseRows = 5;    // workers per round on the dense route
-constexpr int kAggDenseU = 3;       // 16-byte chunks per thread and load on the dense route
+constexpr int kAggDenseRows = 4;    // workers per round on the dense route
+constexpr int kAggDenseU = 2;       // 16-byte chunks per thread and load (sparse and dense routes)
 constexpr int kAggStrip = 4;        // tiles per workgroup: tiles b, b + grid, ...
 static_assert(kAggCols == 8 && kAggHalf == 4 * kBlock, "each thread's columns are one float4 per half");
 
@@ -1095,15 +1095,17 @@ __device__ __forceinline__ void agg_dense_load(DenseChunks &L, const float *__re
                                                const uint32_t *__restrict__ idx, const AggRuns &R, int w0, int w1,
                                                uint32_t q0) {
     const uint32_t a = R.ch_off[w0], e = R.ch_off[w1];
-    const uint32_t o1 = R.ch_off[w0 + 1 < w1 ? w0 + 1 : w1], o2 = R.ch_off[w0 + 2 < w1 ? w0 + 2 : w1],
-                   o3 = R.ch_off[w0 + 3 < w1 ? w0 + 3 : w1], o4 = R.ch_off[w0 + 4 < w1 ? w0 + 4 : w1];
-    static_assert(kAggDenseRows == 5, "the row search below covers five rows");
+    uint32_t o[kAggDenseRows];  // o[j]: the first chunk of row j (rows past w1 start at the end)
+#pragma unroll
+    for (int j = 1; j < kAggDenseRows; ++j) o[j] = R.ch_off[w0 + j < w1 ? w0 + j : w1];
 #pragma unroll
     for (int u = 0; u < kAggDenseU; ++u) {
         const uint32_t Q0 = a + q0 + threadIdx.x + kBlock * u;
         const bool live = Q0 < e;
         const uint32_t Q = live ? Q0 : a;  // past the end: the round's first chunk, masked out
-        const int r = (Q >= o1) + (Q >= o2) + (Q >= o3) + (Q >= o4);
+        int r = 0;
+#pragma unroll
+        for (int j = 1; j < kAggDenseRows; ++j) r += Q >= o[j];
         const int w = w0 + r;
         const uint32_t ql = Q - R.ch_off[w];
         const unsigned long long c = R.ch_c0[w] + ql;
@@ -1169,7 +1171,8 @@ __device__ __forceinline__ void agg_sparse_load(SparseChunks &L, const float *__
     }
 }
 
-__global__ __launch_bounds__(kBlock) void k_topk_agg_tiles(const float *__restrict__ val,
+// four workgroups per CU: at most 128 VGPRs and 40 KB of LDS each
+__global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__restrict__ val,
                                                            const uint32_t *__restrict__ idx, int64_t k, int32_t M,
                                                            const uint32_t *__restrict__ start, int64_t n_t,
                                                            int64_t d, int64_t ld, float *__restrict__ Qhat,
@@ -1261,12 +1264,12 @@ __global__ __launch_bounds__(kBlock) void k_topk_agg_tiles(const float *__restri
                 }
             }
             lds_barrier();
+            const uint32_t base_lo = static_cast<uint32_t>(base);
+            const bool addressable = (static_cast<unsigned long long>(base) >> 32) == 0;  // idx is 32-bit
             if (total <= kAggStage) {
                 for (int c = tid; c < kAggTile; c += kBlock) S.s.mask[c] = 0ull;
                 lds_barrier();
                 // stage every run and mark each entry's worker in its column
-                const uint32_t base_lo = static_cast<uint32_t>(base);
-                const bool addressable = (static_cast<unsigned long long>(base) >> 32) == 0;  // idx is 32-bit
                 for (uint32_t q0 = 0; q0 < R.ch_off[gn]; q0 += kBlock * kAggDenseU) {
                     SparseChunks L;
                     agg_sparse_load(L, val, idx, R, gn, q0);
@@ -1280,8 +1283,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_agg_tiles(const float *__restri
                             const bool in = addressable && c < static_cast<uint32_t>(kAggTile);
                             const int g = L.pos[u] + i;
                             S.s.st_col[g] = in ? static_cast<uint16_t>(c) : static_cast<uint16_t>(0xFFFFu);
-                            S.s.st_w[g] = static_cast<uint8_t>(w);
                             S.s.st_val[g] = elem(L.val[u], i);
+                            S.s.st_w[g] = static_cast<uint8_t>(w);
                             if (in) atomicOr(&S.s.mask[c], 1ull << w);
                         }
                     }
@@ -1339,8 +1342,6 @@ __global__ __launch_bounds__(kBlock) void k_topk_agg_tiles(const float *__restri
                     st4(&S.rows[r][4 * tid], zero);
                     st4(&S.rows[r][kAggHalf + 4 * tid], zero);
                 }
-                const uint32_t base_lo = static_cast<uint32_t>(base);
-                const bool addressable = (static_cast<unsigned long long>(base) >> 32) == 0;  // idx is 32-bit
                 const int n_rounds = (gn + kAggDenseRows - 1) / kAggDenseRows;
                 DenseChunks L;
                 auto load = [&](int w0, uint32_t q0) {

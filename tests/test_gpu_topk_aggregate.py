@@ -3,9 +3,9 @@ messages built on the host, against the oracle's average of the decoded
 messages (the sum in ascending worker order, one division by M), bit for bit
 including the sign of zero.
 
-The messages mix the three kinds of column tiles the kernel tells apart:
-tiles no worker sends anything for, sparse tiles, and dense bands where
-every worker sends a large share of the columns (as the layer-wise gradient
+The messages mix the kinds of column tiles the kernel tells apart: tiles no
+worker sends anything for, tiles with fewer entries than workers, sparse
+tiles, and dense bands where every worker sends a large share of the columns (as the layer-wise gradient
 scales of the large workloads make them).  Values span sixteen decades with
 both signs, so that a sum taken in another order differs.  Worker counts
 cover one, partial rounds of four, one and several groups of 64, and
@@ -100,6 +100,10 @@ CASES = {
     "m65_mixed": (200_000, 65, 3_000, (20_000, 26_000), (100_000, 150_000)),
     "m130_mixed": (100_000, 130, 1_500, (8_000, 12_000), (50_000, 60_000)),
     "m64_sparse": (300_000, 64, 1_000, None, None),
+    # fewer entries per tile than workers (the direct path), next to tiles
+    # that take the other routes
+    "m64_few": (2_000_000, 64, 100, (1_000_000, 1_004_000), None),
+    "m130_few": (1_000_000, 130, 50, (500_000, 502_000), None),
 }
 
 
