@@ -949,7 +949,7 @@ constexpr int kAggGroup = 64;       // workers per group: the bits of a column m
 constexpr int kAggCols = kAggTile / kBlock;  // columns per thread
 constexpr int kAggDenseRows = 4;    // workers per round on the dense route
 constexpr int kAggDenseU = 2;       // 16-byte chunks per thread and load (sparse and dense routes)
-constexpr int kAggStrip = 4;        // tiles per workgroup: tiles b, b + grid, ...
+constexpr int kAggStrip = 4;        // tiles per workgroup (see agg_tile_of)
 static_assert(kAggCols == 8 && kAggHalf == 4 * kBlock, "each thread's columns are one float4 per half");
 
 // column i (0..7) of thread t: 4t + i in the first half, 1024 + 4t + i - 4 in the second
@@ -1171,6 +1171,18 @@ __device__ __forceinline__ void agg_sparse_load(SparseChunks &L, const float *__
     }
 }
 
+// Tile s of workgroup b's strip.  Workgroups go to the 8 XCDs in turn
+// (b % 8) and tiles go to them in blocks of 8 consecutive tiles (block j on
+// XCD j % 8), so that neighbouring tiles, which share the cache lines at
+// their runs' ends and a row of the start table, meet in one L2.  Within
+// an XCD, its i-th workgroup takes the XCD's tiles i, i + per, i + 2 per ...
+// (per = grid / 8), which spreads the dense bands over the workgroups.
+__device__ __forceinline__ int64_t agg_tile_of(int64_t b, int s, int64_t grid) {
+    const int64_t x = b % 8, i = b / 8, per = grid / 8;
+    const int64_t z = i + static_cast<int64_t>(s) * per;
+    return 64 * (z / 8) + 8 * x + (z % 8);
+}
+
 // four workgroups per CU: at most 128 VGPRs and 40 KB of LDS each
 __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__restrict__ val,
                                                            const uint32_t *__restrict__ idx, int64_t k, int32_t M,
@@ -1191,7 +1203,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
     if (n_groups == 1) {
 #pragma unroll
         for (int q = 0; q < kAggStrip; ++q) {
-            const int64_t T = blockIdx.x + static_cast<int64_t>(q) * gridDim.x;
+            const int64_t T = agg_tile_of(blockIdx.x, q, gridDim.x);
             ss[q] = ee[q] = 0u;
             if (T < n_t && lane < M) {
                 ss[q] = start[T * M + lane];
@@ -1203,7 +1215,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
     uint32_t mn[kAggCols];  // unsigned minimum of the terms' bit patterns
     for (int it = 0; it < n_it; ++it) {
         const int sq = it / n_groups;
-        const int64_t T = blockIdx.x + static_cast<int64_t>(sq) * gridDim.x;
+        const int64_t T = agg_tile_of(blockIdx.x, sq, gridDim.x);
         if (T >= n_t) break;  // uniform: the strip's later tiles are past the end too
         const int g0 = (it % n_groups) * kAggGroup;
         const int gn = M - g0 < kAggGroup ? M - g0 : kAggGroup;
@@ -1531,7 +1543,10 @@ hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, flo
     hipLaunchKernelGGL(k_topk_agg_starts, dim3(static_cast<unsigned>(sb), static_cast<unsigned>(D.M)), dim3(kBlock), 0,
                        st, w.idx, D.k, D.M, static_cast<int32_t>(S.n_agg_tiles), S.agg_start);
     const float im = (D.M & (D.M - 1)) == 0 ? 1.0f / static_cast<float>(D.M) : 0.0f;
-    const int64_t nb = (S.n_agg_tiles + kAggStrip - 1) / kAggStrip;
+    // 8 x per workgroups, per large enough that every tile's place in its
+    // XCD's list (at most n_t / 8 + 7) is inside a strip
+    const int64_t per = (S.n_agg_tiles / 8 + 8 + kAggStrip - 1) / kAggStrip;
+    const int64_t nb = 8 * per;
     hipLaunchKernelGGL(k_topk_agg_tiles, dim3(static_cast<unsigned>(nb)), dim3(kBlock), 0, st, w.val, w.idx, D.k, D.M,
                        S.agg_start, S.n_agg_tiles, D.d, D.ld, Qhat, im);
     return hipGetLastError();
