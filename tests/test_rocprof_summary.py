@@ -51,3 +51,26 @@ def test_counter_stats_sum_then_mean(tmp_path):
     assert (k, ctr, n) == ("k_fused_split<1, 4, 4, 8, false>", "FETCH_SIZE", 2) and mean == 60.0
     disp = rs.counter_dispatches(db, "k_fused_split")
     assert [(d["dispatch"], d["grid"], d["FETCH_SIZE"]) for d in disp] == [(7, 4096, 30.0), (9, 4096, 90.0)]
+
+
+def test_per_trial_groups_dispatches(tmp_path):
+    """--per-trial: a kernel's dispatches in launch order, in groups (one per
+    allocation trial); per group the first (warmup) is left out."""
+    path = str(tmp_path / "trials.db")
+    con = sqlite3.connect(path)
+    con.execute("create table kernels (name text, duration integer, start integer, dispatch_id integer)")
+    con.execute("create table counters_collection (kernel_name text, counter_name text, dispatch_id integer, "
+                "value real)")
+    # two trials of 3 dispatches each, a statistics dispatch between them
+    plan = [(FUSED, 9000, 10.0), (FUSED, 2000, 1.0), (FUSED, 4000, 3.0), (STATS, 500, 99.0),
+            (FUSED, 8000, 50.0), (FUSED, 6000, 5.0), (FUSED, 8000, 7.0)]
+    for i, (name, dur, ctr) in enumerate(plan):
+        con.execute("insert into kernels values (?, ?, ?, ?)", (name, dur, 10 * i, 100 + i))
+        for half in (0.25, 0.75):  # two samples per dispatch, summed
+            con.execute("insert into counters_collection values (?, ?, ?, ?)", (name, "X", 100 + i, half * ctr))
+    con.commit()
+    con.close()
+    recs = rs.per_trial(path, "k_fused_split<1, 4, 4, 8, false>", 3)
+    assert [r["trial"] for r in recs] == [0, 1]
+    assert abs(recs[0]["us"] - 3.0) < 1e-9 and abs(recs[1]["us"] - 7.0) < 1e-9
+    assert abs(recs[0]["X"] - 2.0) < 1e-9 and abs(recs[1]["X"] - 6.0) < 1e-9
