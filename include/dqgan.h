@@ -121,6 +121,10 @@ typedef struct dqgan_plan_s *dqgan_plan;
  *   i, in ascending i, each below d.  A message that breaks this (read by
  *   dqgan_unpack or dqgan_aggregate) gives undefined values but no access
  *   outside the buffers: indices at or beyond d are skipped.
+ *   dqgan_aggregate reads both lists in aligned 16-byte words: when M*k*4
+ *   is not a multiple of 16, it also reads (and ignores) the bytes after the
+ *   last entry up to the next 16-byte boundary, so they must be readable
+ *   device memory (as in any allocation made for the buffer itself).
  *   (IDENTITY: val is the dense fp32 [M][ld] p-hat = p.)
  * Unused planes may be NULL. */
 typedef struct {

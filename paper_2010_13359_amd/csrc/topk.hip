@@ -821,11 +821,15 @@ __global__ __launch_bounds__(kBlock) void k_topk_spill_count(const TopkRow *__re
     }
 }
 
-// 7. Per chunk of kTopkChunkTiles tiles (one wave; four chunks per
-// workgroup, independent): the selected candidates of the chunk's run added
-// to its tiles' counts, the tiles' offsets within the chunk (exclusive
-// scan) and the chunk's total.  A fallen-back row's counts come whole from
-// the recount.
+// 7. Per chunk of kTopkChunkTiles tiles: the selected candidates of the
+// chunk's run added to its tiles' counts, the tiles' offsets within the
+// chunk (exclusive scan) and the chunk's total.  A wave takes
+// kScanChunksPerWave consecutive chunks, their counts and runs loaded before
+// the first is examined (one chunk per wave made the launch a hundred
+// thousand tiny workgroups).  A fallen-back row's counts come whole from the
+// recount.
+constexpr int kScanChunksPerWave = 4;
+
 __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__restrict__ rows,
                                                             const uint2 *__restrict__ cand, int64_t cap,
                                                             const uint2 *__restrict__ runs,
@@ -836,51 +840,68 @@ __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__res
     __shared__ uint32_t sel_all[kBlock / 64][kTopkChunkTiles];
     const int m = blockIdx.y;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t c = static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave;
-    if (c >= n_chunks) return;  // whole waves: no barrier below spans waves
+    const int64_t c0 = (static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave) * kScanChunksPerWave;
+    if (c0 >= n_chunks) return;  // whole waves: no barrier below spans waves
     uint32_t *sel = sel_all[wave];
-    const int64_t t = c * kTopkChunkTiles + lane;
     const TopkRow r = rows[m];
-    uint32_t cnt = t < n_tiles ? tile_cnt[static_cast<int64_t>(m) * n_tiles + t] : 0u;
-    if (!r.fallback) {
-        sel[lane] = 0u;
-        __builtin_amdgcn_wave_barrier();
-        const uint2 run = runs[static_cast<int64_t>(m) * n_chunks + c];
-        const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
-        const int64_t first_tile = c * kTopkChunkTiles;
-        // up to 8 of the lane's candidates loaded at once (a run holds at
-        // most 1024)
-        constexpr int kRunU = 8;
-        for (uint32_t j0 = lane; j0 < run.y; j0 += 64 * kRunU) {
-            uint2 cd[kRunU];
+    uint32_t cnt[kScanChunksPerWave];
+    uint2 run[kScanChunksPerWave];
 #pragma unroll
-            for (int u = 0; u < kRunU; ++u) {
-                const uint32_t j = j0 + 64 * u;
-                const int64_t pos = static_cast<int64_t>(run.x) + j;
-                cd[u] = (j < run.y && pos < cap) ? crow[pos] : make_uint2(0u, 0xFFFFFFFFu);
-            }
+    for (int q = 0; q < kScanChunksPerWave; ++q) {
+        const int64_t c = c0 + q;
+        const int64_t t = c * kTopkChunkTiles + lane;
+        cnt[q] = (c < n_chunks && t < n_tiles) ? tile_cnt[static_cast<int64_t>(m) * n_tiles + t] : 0u;
+        run[q] = c < n_chunks ? runs[static_cast<int64_t>(m) * n_chunks + c] : make_uint2(0u, 0u);
+    }
+    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
 #pragma unroll
-            for (int u = 0; u < kRunU; ++u) {
-                if (j0 + 64 * u >= run.y) continue;
-                if (cd[u].x > r.T || (cd[u].x == r.T && cd[u].y <= r.I)) {
-                    const int64_t lt = static_cast<int64_t>(cd[u].y / kTopkTile) - first_tile;
-                    if (lt >= 0 && lt < kTopkChunkTiles) atomicAdd(&sel[lt], 1u);
+    for (int q = 0; q < kScanChunksPerWave; ++q) {
+        const int64_t c = c0 + q;
+        if (c >= n_chunks) break;  // uniform
+        const int64_t t = c * kTopkChunkTiles + lane;
+        uint32_t n_here = cnt[q];
+        if (!r.fallback) {
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            sel[lane] = 0u;
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            const int64_t first_tile = c * kTopkChunkTiles;
+            // up to 8 of the lane's candidates loaded at once (a run holds at
+            // most 1024)
+            constexpr int kRunU = 8;
+            for (uint32_t j0 = lane; j0 < run[q].y; j0 += 64 * kRunU) {
+                uint2 cd[kRunU];
+#pragma unroll
+                for (int u = 0; u < kRunU; ++u) {
+                    const uint32_t j = j0 + 64 * u;
+                    const int64_t pos = static_cast<int64_t>(run[q].x) + j;
+                    cd[u] = (j < run[q].y && pos < cap) ? crow[pos] : make_uint2(0u, 0xFFFFFFFFu);
+                }
+#pragma unroll
+                for (int u = 0; u < kRunU; ++u) {
+                    if (j0 + 64 * u >= run[q].y) continue;
+                    if (cd[u].x > r.T || (cd[u].x == r.T && cd[u].y <= r.I)) {
+                        const int64_t lt = static_cast<int64_t>(cd[u].y / kTopkTile) - first_tile;
+                        if (lt >= 0 && lt < kTopkChunkTiles) atomicAdd(&sel[lt], 1u);
+                    }
                 }
             }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            n_here += sel[lane];
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-        cnt += sel[lane];
-    }
-    uint32_t incl = cnt;
+        uint32_t incl = n_here;
 #pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t v = __shfl_up(incl, o);
-        if (lane >= o) incl += v;
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t v = __shfl_up(incl, o);
+            if (lane >= o) incl += v;
+        }
+        if (t < n_tiles) tile_off[static_cast<int64_t>(m) * n_tiles + t] = incl - n_here;
+        if (lane == 63) chunk_sum[static_cast<int64_t>(m) * n_chunks + c] = incl;
     }
-    if (t < n_tiles) tile_off[static_cast<int64_t>(m) * n_tiles + t] = incl - cnt;
-    if (lane == 63) chunk_sum[static_cast<int64_t>(m) * n_chunks + c] = incl;
 }
 
 // 8. Exclusive scan of the chunk totals of each row (one workgroup per row).
@@ -1511,7 +1532,9 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
                        S.rows, S.fb_hist, S.tile_cnt);
     hipLaunchKernelGGL(k_topk_spill_count, dim3(kSpillBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap,
                        S.tile_cnt, S.n_tiles);
-    hipLaunchKernelGGL(k_topk_count_scan, dim3(static_cast<unsigned>((S.n_chunks + 3) / 4), M), dim3(kBlock), 0, st,
+    const int64_t scan_per_block = (kBlock / 64) * kScanChunksPerWave;
+    hipLaunchKernelGGL(k_topk_count_scan, dim3(static_cast<unsigned>((S.n_chunks + scan_per_block - 1) / scan_per_block), M),
+                       dim3(kBlock), 0, st,
                        S.rows, S.cand,
                        S.cap, S.runs, S.tile_cnt, S.tile_off, S.chunk_sum, S.n_tiles, S.n_chunks);
     hipLaunchKernelGGL(k_topk_chunk_scan, dim3(M), dim3(1024), 0, st, S.rows, S.chunk_sum, S.chunk_off, S.n_chunks);
