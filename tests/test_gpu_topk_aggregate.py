@@ -47,8 +47,9 @@ def _messages(d, M, k, seed, dense_band=None, empty_band=None, dense_share=0.7):
         n_free = k - len(special)
         if dense_band is not None:
             a, b = dense_band
-            nd = min(int(dense_share * n_free), b - a)
-            band = a + rng.choice(b - a, size=nd, replace=False)
+            band_pool = np.setdiff1d(np.arange(a, b), [ALL_NEG0, ALL_BUT_ONE_NEG0, ONE_NEG0])
+            nd = min(int(dense_share * n_free), band_pool.size)
+            band = rng.choice(band_pool, size=nd, replace=False)
             rest_pool = pool.copy()
             rest_pool[a:b] = False
             rest = rng.choice(np.flatnonzero(rest_pool), size=n_free - nd, replace=False)
@@ -104,6 +105,9 @@ CASES = {
     # that take the other routes
     "m64_few": (2_000_000, 64, 100, (1_000_000, 1_004_000), None),
     "m130_few": (1_000_000, 130, 50, (500_000, 502_000), None),
+    # many groups of 64 workers: 16 sparse groups per tile; five dense groups
+    "m1024_sparse": (20_000, 1024, 20, None, None),
+    "m300_dense": (30_000, 300, 10_000, (0, 20_000), None),
 }
 
 
