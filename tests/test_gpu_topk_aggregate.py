@@ -14,7 +14,11 @@ columns: every worker sends -0 (the average is -0), every worker but one
 sends -0 (+0), and one worker alone sends -0 (+0).  The full-size check
 compares the server average of the 64 x 1e6 top-k messages of the largest
 workload with the fused step's, which the parity tests of that workload tie
-to the oracle."""
+to the oracle.  Two checks cover messages outside the format: sorted lists
+ending in indices at or beyond d (skipped, so the average is the oracle's
+over the rest), and unsorted, repeated and out-of-range indices (undefined
+values, but the calls complete, their outputs are finite and the same plan
+then averages a well-formed message exactly)."""
 import numpy as np
 import pytest
 
@@ -154,3 +158,60 @@ def test_topk_average_full_size_equals_fused_step():
     n_bad = int((Qa.view(torch.int32) != Qf.view(torch.int32)).sum())
     plan.close()
     assert same, "%d columns differ" % n_bad
+
+
+def test_topk_average_skips_indices_beyond_d():
+    """Sorted lists whose last entries lie at or beyond d (in the padding
+    [d, ld) and past ld) average as if those entries were not sent."""
+    d, M, k = 100_001, 9, 3_000
+    w = custom(d=d, M=M, kind="topk", k=k, eta=1e-2, seed=62)
+    idx, val = _messages(d, M, k, seed=71, dense_band=(40_000, 44_000))
+    tail = np.array([d, d + 5, w.ld - 1, w.ld, w.ld + 70_000, 2 ** 32 - 1], np.uint32)
+    for m in range(M):
+        # the last len(tail) entries of each list move past d (still ascending)
+        idx[m, -len(tail):] = tail
+    got = _gpu_average(w, idx, val)
+    keep = idx.astype(np.int64) < d
+    ph = np.zeros((M, w.ld), np.float32)
+    for m in range(M):
+        ph[m, idx[m][keep[m]].astype(np.int64)] = val[m][keep[m]]
+    from oracle import oracle as orc
+    exp = np.zeros(w.ld, np.float32)
+    exp[:d] = orc.aggregate(ph, d)
+    assert np.array_equal(got.view(np.uint32), exp.view(np.uint32))
+
+
+def test_topk_malformed_messages_complete_and_leave_the_plan_usable():
+    """Unsorted lists, repeated indices and indices far beyond d give
+    undefined values (the header's contract) but complete without touching
+    memory outside the buffers; the same plan then averages a well-formed
+    message exactly."""
+    import torch
+    from paper_2010_13359_amd import dqgan
+    d, M, k = 50_000, 5, 4_000
+    w = custom(d=d, M=M, kind="topk", k=k, eta=1e-2, seed=63)
+    rng = np.random.default_rng(72)
+    bad_idx = rng.integers(0, 2 ** 32, size=(M, k), dtype=np.uint64).astype(np.uint32)
+    bad_idx[:, ::3] = rng.integers(0, d, size=(M, (k + 2) // 3)).astype(np.uint32)  # in range, unsorted
+    bad_idx[:, 1::7] = 1234  # repeated
+    bad_val = rng.standard_normal((M, k)).astype(np.float32)
+    good_idx, good_val = _messages(d, M, k, seed=73, dense_band=(10_000, 20_000))
+    dev = torch.device("cuda:0")
+    plan = dqgan.Plan.from_workload(w)
+    wire = plan.new_wire(dev)
+    Q = torch.full((w.ld,), float("nan"), dtype=torch.float32, device=dev)
+    Ph = torch.full((M, w.ld), float("nan"), dtype=torch.float32, device=dev)
+    wire.idx.copy_(torch.from_numpy(bad_idx.reshape(-1).view(np.int32)).to(dev))
+    wire.val.copy_(torch.from_numpy(bad_val.reshape(-1)).to(dev))
+    dqgan.aggregate(plan, wire, Q)
+    dqgan.unpack(plan, wire, Ph)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(Q).all()) and bool(torch.isfinite(Ph).all())
+    wire.idx.copy_(torch.from_numpy(good_idx.reshape(-1).view(np.int32)).to(dev))
+    wire.val.copy_(torch.from_numpy(good_val.reshape(-1)).to(dev))
+    dqgan.aggregate(plan, wire, Q)
+    torch.cuda.synchronize()
+    got = Q.cpu().numpy()
+    plan.close()
+    exp = _oracle_average(w, good_idx, good_val)
+    assert np.array_equal(got.view(np.uint32), exp.view(np.uint32))
