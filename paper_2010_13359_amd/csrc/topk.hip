@@ -952,8 +952,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_scatter(const float *__restrict
 //  - dense: rounds of kAggDenseRows workers.  A round's runs are read in
 //    aligned 16-byte chunks and scattered to one LDS row per worker (a
 //    column without an entry holds +0); each thread adds its columns of the
-//    rows in worker order, then clears them.  The next round's first chunks
-//    are loaded before the current round is summed.
+//    rows in worker order, then clears them.  A round's first chunks are
+//    loaded two rounds ahead, into one of two sets of registers.
 // The sums start from +0.  A partial sum started from +0 is never -0, so
 // adding the +0 of a worker without an entry changes nothing, and the sum
 // over the present entries equals the definition's sum over all M decoded
@@ -969,7 +969,8 @@ constexpr int kAggStage = 1536;     // entries of a group staged on the sparse r
 constexpr int kAggGroup = 64;       // workers per group: the bits of a column mask
 constexpr int kAggCols = kAggTile / kBlock;  // columns per thread
 constexpr int kAggDenseRows = 4;    // workers per round on the dense route
-constexpr int kAggDenseU = 2;       // 16-byte chunks per thread and load (sparse and dense routes)
+constexpr int kAggSparseU = 2;      // 16-byte chunks per thread and load on the sparse route
+constexpr int kAggDenseU = 1;       // ... and on the dense route, which keeps two such loads in flight
 constexpr int kAggStrip = 4;        // tiles per workgroup (see agg_tile_of)
 static_assert(kAggCols == 8 && kAggHalf == 4 * kBlock, "each thread's columns are one float4 per half");
 
@@ -996,13 +997,20 @@ __device__ __forceinline__ uint32_t u4_at(const uint4 &v, int i) {
 
 __global__ __launch_bounds__(kBlock) void k_topk_agg_starts(const uint32_t *__restrict__ idx, int64_t k, int32_t M,
                                                             int32_t n_t, uint32_t *__restrict__ start) {
-    const int m = blockIdx.y;
+    // Workgroup b takes segment b / M of a row.  The M workgroups of a
+    // segment are consecutive, and with M a multiple of 8 the XCD of b
+    // (b % 8) takes M / 8 consecutive rows: a tile's M starts are written
+    // close in time, each contiguous eighth of them from one L2, which merges
+    // the 4-byte stores before they reach HBM.
+    const int64_t b = blockIdx.x;
+    const int seg = static_cast<int>(b / M), t = static_cast<int>(b % M);
+    const int m = M % 8 == 0 ? (t % 8) * (M / 8) + t / 8 : t;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t row0 = static_cast<int64_t>(m) * k;  // flat index of the row's first entry
     const int64_t c_first = row0 >> 2;
     const int64_t c_last = (row0 + k - 1) >> 2;               // the last chunk holding an entry of the row
     const int64_t n_ch = ((row0 + k) >> 2) - c_first + 1;     // ... and the chunk of the end (entry k)
-    const int64_t cw = (static_cast<int64_t>(blockIdx.x) * (kBlock / 64) + wave) * (64 * kStartsLoads);
+    const int64_t cw = (static_cast<int64_t>(seg) * (kBlock / 64) + wave) * (64 * kStartsLoads);
     if (cw >= n_ch) return;
     const uint4 *chunks = reinterpret_cast<const uint4 *>(idx);
     uint4 v[kStartsLoads];
@@ -1157,10 +1165,10 @@ __device__ __forceinline__ void agg_dense_scatter(const DenseChunks &L, AggLds &
 // the whole group (chunks 0 .. ch_off[gn]), with the stage position of the
 // chunk's entry 0 and a 4-bit mask of the entries that belong to the run.
 struct SparseChunks {
-    uint4 idx[kAggDenseU];
-    f32x4 val[kAggDenseU];
-    int pos[kAggDenseU];       // stage position of entry 0 (entries 1..3 follow)
-    uint32_t tag[kAggDenseU];  // bits 0..3: entries of the run; bits 4..: worker in the group
+    uint4 idx[kAggSparseU];
+    f32x4 val[kAggSparseU];
+    int pos[kAggSparseU];       // stage position of entry 0 (entries 1..3 follow)
+    uint32_t tag[kAggSparseU];  // bits 0..3: entries of the run; bits 4..: worker in the group
 };
 
 __device__ __forceinline__ void agg_sparse_load(SparseChunks &L, const float *__restrict__ val,
@@ -1168,7 +1176,7 @@ __device__ __forceinline__ void agg_sparse_load(SparseChunks &L, const float *__
                                                 uint32_t q0) {
     const uint32_t e = R.ch_off[gn];
 #pragma unroll
-    for (int u = 0; u < kAggDenseU; ++u) {
+    for (int u = 0; u < kAggSparseU; ++u) {
         const uint32_t Q0 = q0 + threadIdx.x + kBlock * u;
         const bool live = Q0 < e;
         const uint32_t Q = live ? Q0 : 0u;  // past the end: the group's first chunk, masked out
@@ -1303,11 +1311,11 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                 for (int c = tid; c < kAggTile; c += kBlock) S.s.mask[c] = 0ull;
                 lds_barrier();
                 // stage every run and mark each entry's worker in its column
-                for (uint32_t q0 = 0; q0 < R.ch_off[gn]; q0 += kBlock * kAggDenseU) {
+                for (uint32_t q0 = 0; q0 < R.ch_off[gn]; q0 += kBlock * kAggSparseU) {
                     SparseChunks L;
                     agg_sparse_load(L, val, idx, R, gn, q0);
 #pragma unroll
-                    for (int u = 0; u < kAggDenseU; ++u) {
+                    for (int u = 0; u < kAggSparseU; ++u) {
                         const uint32_t w = L.tag[u] >> 4;
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
@@ -1376,28 +1384,28 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                     st4(&S.rows[r][kAggHalf + 4 * tid], zero);
                 }
                 const int n_rounds = (gn + kAggDenseRows - 1) / kAggDenseRows;
-                DenseChunks L;
-                auto load = [&](int w0, uint32_t q0) {
+                // two sets of chunk registers: round r's first chunks are
+                // loaded during round r - 2
+                DenseChunks La, Lb;
+                auto load = [&](DenseChunks &L, int w0, uint32_t q0) {
                     const int w1 = w0 + kAggDenseRows < gn ? w0 + kAggDenseRows : gn;
-                    if (R.ch_off[w1] - R.ch_off[w0] > q0) {
+                    if (w0 < gn && R.ch_off[w1] - R.ch_off[w0] > q0) {
                         agg_dense_load(L, val, idx, R, w0, w1, q0);
                     } else {
 #pragma unroll
                         for (int u = 0; u < kAggDenseU; ++u) L.tag[u] = 0u;
                     }
                 };
-                load(0, 0u);
-                lds_barrier();  // the rows are cleared before the first scatter
-                for (int r = 0; r < n_rounds; ++r) {
+                auto round = [&](DenseChunks &L, int r) {
                     const int w0 = r * kAggDenseRows;
                     const int w1 = w0 + kAggDenseRows < gn ? w0 + kAggDenseRows : gn;
                     const uint32_t nch = R.ch_off[w1] - R.ch_off[w0];
                     agg_dense_scatter(L, S, base_lo, addressable);
                     for (uint32_t q0 = kBlock * kAggDenseU; q0 < nch; q0 += kBlock * kAggDenseU) {
-                        load(w0, q0);
+                        load(L, w0, q0);
                         agg_dense_scatter(L, S, base_lo, addressable);
                     }
-                    if (r + 1 < n_rounds) load(w1, 0u);
+                    if (r + 2 < n_rounds) load(L, w0 + 2 * kAggDenseRows, 0u);
                     lds_barrier();
                     for (int rr = 0; rr < w1 - w0; ++rr) {
                         const f32x4 x0 = ld4(&S.rows[rr][4 * tid]), x1 = ld4(&S.rows[rr][kAggHalf + 4 * tid]);
@@ -1412,6 +1420,13 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                         st4(&S.rows[rr][kAggHalf + 4 * tid], zero);
                     }
                     lds_barrier();
+                };
+                load(La, 0, 0u);
+                load(Lb, kAggDenseRows, 0u);
+                lds_barrier();  // the rows are cleared before the first scatter
+                for (int r = 0; r < n_rounds; r += 2) {
+                    round(La, r);
+                    if (r + 1 < n_rounds) round(Lb, r + 1);
                 }
             }
             lds_barrier();  // the next pair rewrites the group's tables and the LDS buffers
@@ -1563,7 +1578,7 @@ hipError_t launch_topk_aggregate(const dqgan_plan_s &P, const dqgan_wire &w, flo
     // a row spans at most k / 4 + 2 chunks, its end included
     const int64_t per_block = static_cast<int64_t>(kBlock) * kStartsLoads;
     const int64_t sb = (D.k / 4 + 2 + per_block - 1) / per_block;
-    hipLaunchKernelGGL(k_topk_agg_starts, dim3(static_cast<unsigned>(sb), static_cast<unsigned>(D.M)), dim3(kBlock), 0,
+    hipLaunchKernelGGL(k_topk_agg_starts, dim3(static_cast<unsigned>(sb * D.M)), dim3(kBlock), 0,
                        st, w.idx, D.k, D.M, static_cast<int32_t>(S.n_agg_tiles), S.agg_start);
     const float im = (D.M & (D.M - 1)) == 0 ? 1.0f / static_cast<float>(D.M) : 0.0f;
     // 8 x per workgroups, per large enough that every tile's place in its
