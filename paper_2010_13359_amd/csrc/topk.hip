@@ -954,15 +954,15 @@ __global__ __launch_bounds__(kBlock) void k_topk_scatter(const float *__restrict
 //    column without an entry holds +0); each thread adds its columns of the
 //    rows in worker order, then clears them.  A round's first chunks are
 //    loaded two rounds ahead, into one of two sets of registers.
-// The sums start from +0.  A partial sum started from +0 is never -0, so
-// adding the +0 of a worker without an entry changes nothing, and the sum
-// over the present entries equals the definition's sum over all M decoded
-// rows, except in one case: every worker sent -0 for the column, where the
-// definition gives -0.  That is the case exactly when the sum is +0 and
-// every one of the M terms has its sign bit set, which the unsigned minimum
-// of the terms' bit patterns (a worker without an entry counting as +0)
-// tells.  Indices outside the tile, and runs longer than the tile (only a
-// malformed message has them), are skipped and cut to the tile's width.
+// The sums start from -0: fl(-0 + x) = x for every x, so starting there
+// gives the definition's sum, which starts from worker 0's term.  In round
+// to nearest a partial sum is -0 exactly while every term so far is -0, and
+// adding +0 changes a partial sum only when it is -0 (to +0).  So the +0
+// terms of workers without an entry can be added at any point of the chain:
+// the dense route adds them in place (cleared row entries), the sparse
+// route adds one +0 for a column that a worker of the group did not send.
+// Indices outside the tile, and runs longer than the tile (only a malformed
+// message has them), are skipped and cut to the tile's width.
 constexpr int kAggTile = 2048;      // columns per tile
 constexpr int kAggHalf = kAggTile / 2;
 constexpr int kAggStage = 1536;     // entries of a group staged on the sparse route
@@ -1241,7 +1241,6 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
         }
     }
     float acc[kAggCols];
-    uint32_t mn[kAggCols];  // unsigned minimum of the terms' bit patterns
     for (int it = 0; it < n_it; ++it) {
         const int sq = it / n_groups;
         const int64_t T = agg_tile_of(blockIdx.x, sq, gridDim.x);
@@ -1251,10 +1250,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
         const int64_t base = T * kAggTile;
         if (g0 == 0) {
 #pragma unroll
-            for (int i = 0; i < kAggCols; ++i) {
-                acc[i] = 0.0f;
-                mn[i] = 0xFFFFFFFFu;
-            }
+            for (int i = 0; i < kAggCols; ++i) acc[i] = -0.0f;
         }
         uint32_t s_raw = 0u, e_raw = 0u;
         if (n_groups == 1) {
@@ -1280,7 +1276,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
         const uint32_t total = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(incl), 63));
         if (total == 0u) {
 #pragma unroll
-            for (int i = 0; i < kAggCols; ++i) mn[i] = 0u;  // every term is +0
+            for (int i = 0; i < kAggCols; ++i) acc[i] = add_rn(acc[i], 0.0f);  // the group's terms are +0
         } else {
             // the group's runs, their offsets and chunks, for every wave (wave 0 writes them)
             if (wave == 0) {
@@ -1367,13 +1363,8 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
 #pragma unroll
                 for (int i = 0; i < kAggCols; ++i) {
                     const uint32_t b = S.s.col_base[agg_col(tid, i)];
-                    uint32_t m = cnt[i] == static_cast<uint32_t>(gn) ? mn[i] : 0u;  // an absent worker: +0
-                    for (uint32_t q = 0; q < cnt[i]; ++q) {
-                        const float x = S.s.placed[b + q];
-                        acc[i] = add_rn(acc[i], x);
-                        m = min(m, __float_as_uint(x));
-                    }
-                    mn[i] = m;
+                    for (uint32_t q = 0; q < cnt[i]; ++q) acc[i] = add_rn(acc[i], S.s.placed[b + q]);
+                    if (cnt[i] != static_cast<uint32_t>(gn)) acc[i] = add_rn(acc[i], 0.0f);  // an absent worker's +0
                 }
             } else {
                 // the rows start cleared; each thread clears its own columns
@@ -1413,8 +1404,6 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                         for (int c = 0; c < 4; ++c) {
                             acc[c] = add_rn(acc[c], elem(x0, c));
                             acc[c + 4] = add_rn(acc[c + 4], elem(x1, c));
-                            mn[c] = min(mn[c], __float_as_uint(elem(x0, c)));
-                            mn[c + 4] = min(mn[c + 4], __float_as_uint(elem(x1, c)));
                         }
                         st4(&S.rows[rr][4 * tid], zero);
                         st4(&S.rows[rr][kAggHalf + 4 * tid], zero);
@@ -1440,9 +1429,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                     f32x4 q;
 #pragma unroll
                     for (int c = 0; c < 4; ++c) {
-                        const int i = 4 * h + c;
-                        const bool neg0 = __float_as_uint(acc[i]) == 0u && mn[i] >= 0x80000000u;
-                        const float sacc = neg0 ? -0.0f : acc[i];
+                        const float sacc = acc[4 * h + c];
                         set_elem(q, c, col + c >= d ? 0.0f
                                        : invM > 0.0f ? mul_rn(sacc, invM)
                                                      : static_cast<float>(static_cast<double>(sacc) /
