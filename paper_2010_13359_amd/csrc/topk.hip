@@ -1099,13 +1099,13 @@ union AggLds {
     float rows[kAggDenseRows][kAggTile];    // dense route: one row per worker of a round
 };
 
-// A group's runs as the dense route reads them: worker w's run starts at
+// A group's runs as both routes read them: worker w's run starts at
 // entry G0 = (g0 + w) * k + start of the flat [M][k] lists; its chunks are
 // the 16-byte words c0 .. c0 + nc - 1 with c0 = G0 / 4, and the run's first
 // entry is entry lo = G0 % 4 of chunk c0.  ch_off is the exclusive prefix of
 // the chunk counts over the group.
 struct AggRuns {
-    uint32_t run_s[kAggGroup], woff[kAggGroup + 1];
+    uint32_t woff[kAggGroup + 1];  // exclusive prefix of the run lengths
     unsigned long long ch_c0[kAggGroup];
     uint32_t ch_off[kAggGroup + 1];
     uint32_t ch_lo[kAggGroup];
@@ -1290,7 +1290,6 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                     const uint32_t y = __shfl_up(cincl, o);
                     if (lane >= o) cincl += y;
                 }
-                R.run_s[lane] = static_cast<uint32_t>(s0);
                 R.woff[lane] = incl - rn;
                 R.ch_c0[lane] = c0;
                 R.ch_off[lane] = cincl - nc;
