@@ -1,4 +1,5 @@
-"""Iterations of Algorithm 2 captured in a HIP graph and replayed.
+"""Iterations of Algorithm 2, and the server side as separate calls,
+captured in a HIP graph and replayed.
 
 The two passes (dqgan_step_scales, dqgan_step_apply) issue kernel launches
 only (no memset, no host synchronisation), so a caller can capture several
@@ -79,3 +80,44 @@ def test_graph_replay_equals_eager(name):
             assert np.array_equal(a.view(np.uint32), b.view(np.uint32)), "replay %d differs in %s" % (rep, key)
     del graph
     s.close()
+
+
+SERVER_CASES = {
+    "qsgd15_m32_segs": CASES["qsgd15_m32_segs"],
+    "mbit8_linf_m13": CASES["mbit8_linf_m13"],
+    "topk_m11": CASES["topk_m11"],
+    # several column tiles of the top-k average, dense and sparse ones
+    "topk_m64_tiles": lambda: custom(d=50001, M=64, kind="topk", k=3000, eta=1e-2, seed=26),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SERVER_CASES))
+def test_graph_replay_server_calls_equal_eager(name):
+    """The server side as separate calls (dqgan_aggregate, then
+    dqgan_unpack) captured in a graph: every replay, after the outputs are
+    overwritten, reproduces the eager results bit for bit."""
+    import torch
+    w = SERVER_CASES[name]()
+    print("case", name, "d", w.d, "M", w.M, flush=True)
+    G, E, W = inputs(w)
+    s = GpuState(w, G, E, W)
+    s.fused(1)  # a message to average
+    Ph = torch.full((w.M, w.ld), float("nan"), dtype=torch.float32, device=s.Q.device)
+    s.dq.aggregate(s.plan, s.wire, s.Q)
+    s.dq.unpack(s.plan, s.wire, Ph)
+    torch.cuda.synchronize()
+    q_ref, ph_ref = s.Q.cpu().numpy(), Ph.cpu().numpy()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        s.dq.aggregate(s.plan, s.wire, s.Q)
+        s.dq.unpack(s.plan, s.wire, Ph)
+    torch.cuda.synchronize()
+    for rep in range(REPLAYS):
+        s.Q.fill_(float("nan"))
+        Ph.fill_(float("nan"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(s.Q.cpu().numpy().view(np.uint32), q_ref.view(np.uint32)), "replay %d: q-hat" % rep
+        assert np.array_equal(Ph.cpu().numpy().view(np.uint32), ph_ref.view(np.uint32)), "replay %d: p-hat" % rep
+    del graph
