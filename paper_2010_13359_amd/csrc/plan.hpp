@@ -46,7 +46,8 @@ constexpr double kInfinityCacheBytes = 256.0 * 1024 * 1024;
 // key > T, or key == T and i <= I.
 struct TopkRow {
     uint32_t lo, hi;     // candidate band [lo, hi] of keys, from the sample
-    uint32_t n_cand;     // candidates staged into the row's list by the full pass (may exceed the capacity)
+    uint32_t n_cand;     // candidates staged into the row's list by the full pass (may exceed the capacity);
+                         // this and n_spill, n_above are counted in TopkScratch::ctr and copied here
     uint32_t fallback;   // 1: the band missed the k-th key; the full-row search decides
     uint32_t T, I;       // the selection
     uint32_t n_spill;    // candidates a wave could not stage: stored from the top of the row's list down
@@ -59,6 +60,13 @@ struct TopkRow {
 };
 
 constexpr int kTopkTile = 256;            // elements per counting tile (one wave of quads)
+// The full pass's counters of a row live in their own block of
+// TopkScratch::ctr, not in the row's TopkRow: every workgroup of the pass
+// reads its row's band from rows[m] when it starts, and the other
+// workgroups' atomics on the same cache line held the pass 0.3 ms back at
+// 64 rows of 10^8.  The first search kernel copies them into rows[m].
+constexpr int kRowCtrWords = 64;          // words per row (one 256-byte block)
+constexpr int kCtrCand = 0, kCtrAbove = 1, kCtrSpill = 2;
 constexpr int kTopkChunkTiles = 64;       // tiles per workgroup of the full pass: one candidate run each
 constexpr int kSampleBins = 32768;        // sample histogram: key >> 16 (keys < 2^31)
 constexpr int64_t kSampleStride = 65536;  // one 256-element chunk sampled per 65536 elements
@@ -68,6 +76,7 @@ constexpr int kSelectPasses = 6;          // histogram slots of a search: up to 
 // Top-k workspace (one set per plan).
 struct TopkScratch {
     TopkRow *rows = nullptr;        // [M]
+    uint32_t *ctr = nullptr;        // [M][kRowCtrWords] the full pass's counters of each row, apart from rows
     uint32_t *hist = nullptr;       // [M][kSampleBins] sample histogram (zero between iterations)
     uint32_t *sel_hist = nullptr;   // [M][kDigitBins] histogram of the first key digit among the candidates
     uint2 *play = nullptr;          // [M][cap] the candidates in play after the first key digit

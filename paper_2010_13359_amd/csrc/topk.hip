@@ -203,8 +203,8 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *w
 // 2. Band: the sample ranks k/d * s -+ 8 sigma (binomial) bracket the k-th
 // key; the bins where the count from the top reaches them bound [lo, hi].
 __global__ __launch_bounds__(1024) void k_topk_band(uint32_t *__restrict__ hist, uint32_t *__restrict__ sel_hist,
-                                                    TopkRow *__restrict__ rows, uint32_t n_samples, int64_t d,
-                                                    int64_t k) {
+                                                    TopkRow *__restrict__ rows, uint32_t *__restrict__ ctr,
+                                                    uint32_t n_samples, int64_t d, int64_t k) {
     // thread t holds the t-th group of kPer bins counted from the top; a
     // block scan finds the group where the count from the top reaches a
     // rank, and that thread finds the bin in its registers.
@@ -271,6 +271,8 @@ __global__ __launch_bounds__(1024) void k_topk_band(uint32_t *__restrict__ hist,
         row.lo = lo;
         row.hi = hi;
         rows[m] = row;
+        uint32_t *c = ctr + static_cast<int64_t>(m) * kRowCtrWords;
+        c[kCtrCand] = c[kCtrAbove] = c[kCtrSpill] = 0u;
     }
 }
 
@@ -282,9 +284,10 @@ __global__ __launch_bounds__(1024) void k_topk_band(uint32_t *__restrict__ hist,
 // 16 counts with one 64-byte store at the end: over 64 rows of 10^8 elements
 // a 4-byte count store per tile held the pass 8 % above its loads alone.
 // Candidates are staged in the wave's quarter of an LDS buffer with a
-// wave-uniform count; at the end the workgroup adds its above-band total to
-// the row and writes its candidates as one run from the bottom of the row's
-// list, whose place it records for the per-chunk count.  A tile whose
+// wave-uniform count; at the end the workgroup adds its above-band total
+// (the sum of its tile counts) to the row's counters and writes its
+// candidates as one run from the bottom of the row's list, whose place it
+// records for the per-chunk count.  A tile whose
 // candidates do not fit the wave's quarter (more than 256 in-band keys in
 // its 4096 elements: a segment whose scale puts most of it in the band)
 // stores them from the top of the list down ("spills").  A tile wholly below d
@@ -295,9 +298,9 @@ constexpr int kPassTilesPerWave = 4 * kPassRounds;
 constexpr int kPassTilesPerBlock = kPassTilesPerWave * (kBlock / 64);
 __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
-                                                      TopkRow *__restrict__ rows, uint32_t *__restrict__ tile_cnt,
-                                                      uint2 *__restrict__ cand, int64_t cap, uint2 *__restrict__ runs,
-                                                      int64_t n_chunks) {
+                                                      const TopkRow *__restrict__ rows, uint32_t *__restrict__ ctr,
+                                                      uint32_t *__restrict__ tile_cnt, uint2 *__restrict__ cand,
+                                                      int64_t cap, uint2 *__restrict__ runs, int64_t n_chunks) {
     constexpr uint32_t kStage = 256;  // staged candidates per wave
     constexpr int kWaves = kBlock / 64;
     __shared__ uint2 buf[kWaves][kStage];
@@ -313,7 +316,6 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     uint2 *stage = buf[wave];
     const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kPassTilesPerBlock + kPassTilesPerWave * wave;
     uint32_t my_cnt = 0;  // lane j < 16: above-band count of tile t0 + j
-    uint32_t nab = 0;     // wave-uniform: keys above the band in the wave's tiles
     uint32_t ns = 0;      // wave-uniform: candidates staged by the wave
     for (int round = 0; round < kPassRounds; ++round) {
         // Unconditional loads (a tile past the row's end reads the last tile
@@ -359,7 +361,6 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                 }
             }
             my_cnt = lane == 4 * round + it ? above_n : my_cnt;
-            nab += above_n;
             if (tot) {
                 // this lane's first slot: the wave's candidates in lower lanes
                 uint32_t pre = 0;
@@ -380,7 +381,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                     // the wave's staging is full: these go to the top of the
                     // row's list, counted per tile by k_topk_spill_count
                     uint32_t sbase = 0;
-                    if (lane == 0) sbase = atomicAdd(&rows[m].n_spill, tot);
+                    if (lane == 0) sbase = atomicAdd(ctr + static_cast<int64_t>(m) * kRowCtrWords + kCtrSpill, tot);
                     sbase = __builtin_amdgcn_readfirstlane(sbase);
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
@@ -396,6 +397,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     }
     // the wave's 16 tile counts: lanes 0..15, one contiguous store
     if (lane < kPassTilesPerWave && t0 + lane < n_tiles) tile_cnt[static_cast<int64_t>(m) * n_tiles + t0 + lane] = my_cnt;
+    // keys above the band in the wave's tiles: the sum of its 16 tile counts
+    uint32_t nab = my_cnt;
+#pragma unroll
+    for (int o = 1; o < kPassTilesPerWave; o <<= 1) nab += __shfl_xor(nab, o);
     if (lane == 0) {
         wave_nab[wave] = nab;
         wave_ns[wave] = ns;
@@ -408,8 +413,9 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
             a += wave_nab[w];
             n += wave_ns[w];
         }
-        if (a) atomicAdd(&rows[m].n_above, a);
-        base = n ? atomicAdd(&rows[m].n_cand, n) : 0u;
+        uint32_t *c = ctr + static_cast<int64_t>(m) * kRowCtrWords;
+        if (a) atomicAdd(c + kCtrAbove, a);
+        base = n ? atomicAdd(c + kCtrCand, n) : 0u;
         runs[static_cast<int64_t>(m) * n_chunks + blockIdx.x] = make_uint2(base, n);
     }
     __syncthreads();
@@ -478,12 +484,22 @@ __device__ TopState sel_first_digit(const TopkRow &r, int64_t k, const uint32_t 
 constexpr int kSelU = 8;  // candidates in flight per thread
 
 // The first key digit's histogram (kSelBlocks workgroups per row).
-__global__ __launch_bounds__(kBlock) void k_topk_sel_top(const TopkRow *__restrict__ rows,
+__global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ rows, const uint32_t *__restrict__ ctr,
                                                          const uint2 *__restrict__ cand, int64_t cap, int64_t k,
                                                          uint32_t *__restrict__ sel_hist) {
     __shared__ uint32_t h[kDigitBins];
     const int m = blockIdx.y;
-    const TopkRow r = rows[m];
+    TopkRow r = rows[m];
+    const uint32_t *c = ctr + static_cast<int64_t>(m) * kRowCtrWords;
+    r.n_cand = c[kCtrCand];
+    r.n_above = c[kCtrAbove];
+    r.n_spill = c[kCtrSpill];
+    // the later kernels read the counters from the row record
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        rows[m].n_cand = r.n_cand;
+        rows[m].n_above = r.n_above;
+        rows[m].n_spill = r.n_spill;
+    }
     const int width = key_width(r);
     if (!sel_ok(r, k, cap) || width == 0) return;
     const int wbits = width < 11 ? width : 11;
@@ -1466,6 +1482,7 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
     const size_t M = static_cast<size_t>(D.M);
     const size_t digit_words = M * kSelectPasses * kDigitBins;
     hipError_t e = hipMalloc(reinterpret_cast<void **>(&S.rows), M * sizeof(TopkRow));
+    if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.ctr), M * kRowCtrWords * sizeof(uint32_t));
     if (e == hipSuccess) e = hipMalloc(reinterpret_cast<void **>(&S.hist), M * kSampleBins * sizeof(uint32_t));
     // the sample histogram starts at zero; every iteration zeroes it again once read
     if (e == hipSuccess) e = hipMemset(S.hist, 0, M * kSampleBins * sizeof(uint32_t));
@@ -1495,6 +1512,7 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
 void topk_free(dqgan_plan_s &P) {
     TopkScratch &S = P.topk;
     (void)hipFree(S.rows);
+    (void)hipFree(S.ctr);
     (void)hipFree(S.hist);
     (void)hipFree(S.sel_hist);
     (void)hipFree(S.fb_hist);
@@ -1517,10 +1535,11 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < kSampleBlocks ? sb : kSampleBlocks), M),
                        dim3(kSampleThreads), 0, st,
                        G, E, eta, D.d, D.ld, S.n_sample_chunks, S.hist);
-    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.sel_hist, S.rows, S.n_samples, D.d, D.k);
+    hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.sel_hist, S.rows, S.ctr, S.n_samples, D.d,
+                       D.k);
     hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>(S.n_chunks), M), dim3(kBlock), 0, st, G, E, eta, D.d,
-                       D.ld, S.n_tiles, S.rows, S.tile_cnt, S.cand, S.cap, S.runs, S.n_chunks);
-    hipLaunchKernelGGL(k_topk_sel_top, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, D.k,
+                       D.ld, S.n_tiles, S.rows, S.ctr, S.tile_cnt, S.cand, S.cap, S.runs, S.n_chunks);
+    hipLaunchKernelGGL(k_topk_sel_top, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, S.cand, S.cap, D.k,
                        S.sel_hist);
     hipLaunchKernelGGL(k_topk_sel_collect, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, D.k,
                        S.sel_hist, S.play);
