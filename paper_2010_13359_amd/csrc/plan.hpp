@@ -52,7 +52,7 @@ struct TopkRow {
     uint32_t T, I;       // the selection
     uint32_t n_spill;    // candidates a wave could not stage: stored from the top of the row's list down
     uint32_t slots;      // bit p: the candidate search built digit histogram p in this iteration
-    uint32_t n_play;     // candidates still in play after the first key digit, listed for the finish
+    uint32_t pad1;
     uint32_t pad0;
     uint32_t total;      // selected count found by the tile scan (equals k)
     uint32_t n_above;    // keys above the band, counted by the full pass
@@ -60,13 +60,15 @@ struct TopkRow {
 };
 
 constexpr int kTopkTile = 256;            // elements per counting tile (one wave of quads)
-// The full pass's counters of a row live in their own block of
-// TopkScratch::ctr, not in the row's TopkRow: every workgroup of the pass
-// reads its row's band from rows[m] when it starts, and the other
-// workgroups' atomics on the same cache line held the pass 0.3 ms back at
-// 64 rows of 10^8.  The first search kernel copies them into rows[m].
+// The counters that many workgroups of one kernel update atomically live in
+// their own block of TopkScratch::ctr, not in the row's TopkRow: every
+// workgroup of the full pass reads its row's band from rows[m] when it
+// starts, and the other workgroups' atomics on the same cache line held the
+// pass 0.3 ms back at 64 rows of 10^8.  The first search kernel copies the
+// pass's counters into rows[m]; the finish reads the play count here.
 constexpr int kRowCtrWords = 64;          // words per row (one 256-byte block)
 constexpr int kCtrCand = 0, kCtrAbove = 1, kCtrSpill = 2;
+constexpr int kCtrPlay = 3;  // candidates still in play after the first key digit, listed for the finish
 constexpr int kTopkChunkTiles = 64;       // tiles per workgroup of the full pass: one candidate run each
 constexpr int kSampleBins = 32768;        // sample histogram: key >> 16 (keys < 2^31)
 constexpr int64_t kSampleStride = 65536;  // one 256-element chunk sampled per 65536 elements

@@ -272,7 +272,7 @@ __global__ __launch_bounds__(1024) void k_topk_band(uint32_t *__restrict__ hist,
         row.hi = hi;
         rows[m] = row;
         uint32_t *c = ctr + static_cast<int64_t>(m) * kRowCtrWords;
-        c[kCtrCand] = c[kCtrAbove] = c[kCtrSpill] = 0u;
+        c[kCtrCand] = c[kCtrAbove] = c[kCtrSpill] = c[kCtrPlay] = 0u;
     }
 }
 
@@ -530,7 +530,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ r
 
 // The candidates in the first digit's bin, listed (kSelBlocks workgroups per
 // row; one atomic per wave and round).
-__global__ __launch_bounds__(kBlock) void k_topk_sel_collect(TopkRow *__restrict__ rows,
+__global__ __launch_bounds__(kBlock) void k_topk_sel_collect(const TopkRow *__restrict__ rows,
+                                                             uint32_t *__restrict__ ctr,
                                                              const uint2 *__restrict__ cand, int64_t cap, int64_t k,
                                                              const uint32_t *__restrict__ sel_hist,
                                                              uint2 *__restrict__ play) {
@@ -571,7 +572,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_collect(TopkRow *__restrict
         }
         if (tot) {
             uint32_t base = 0;
-            if (lane == 0) base = atomicAdd(&rows[m].n_play, tot);
+            if (lane == 0) base = atomicAdd(ctr + static_cast<int64_t>(m) * kRowCtrWords + kCtrPlay, tot);
             base = __builtin_amdgcn_readfirstlane(base);
 #pragma unroll
             for (int u = 0; u < kSelU; ++u) {
@@ -604,7 +605,8 @@ __device__ __forceinline__ void block_find(const uint32_t *h, int nb, uint32_t r
     __syncthreads();
 }
 
-__global__ __launch_bounds__(1024) void k_topk_sel_finish(TopkRow *__restrict__ rows, int64_t cap, int64_t k,
+__global__ __launch_bounds__(1024) void k_topk_sel_finish(TopkRow *__restrict__ rows, const uint32_t *__restrict__ ctr,
+                                                          int64_t cap, int64_t k,
                                                           const uint32_t *__restrict__ sel_hist,
                                                           const uint2 *__restrict__ play,
                                                           uint32_t *__restrict__ fb_hist) {
@@ -627,7 +629,8 @@ __global__ __launch_bounds__(1024) void k_topk_sel_finish(TopkRow *__restrict__ 
     uint32_t rank = st.rank, kp = st.kp;
     int top = st.top;
     const uint2 *prow = play + static_cast<int64_t>(m) * cap;
-    const uint32_t n = r.n_play < cap ? r.n_play : static_cast<uint32_t>(cap);
+    const uint32_t n_play = ctr[static_cast<int64_t>(m) * kRowCtrWords + kCtrPlay];
+    const uint32_t n = n_play < cap ? n_play : static_cast<uint32_t>(cap);
     uint32_t n_bin = n;
     // remaining digits of key - lo
     while (top > 0) {
@@ -1541,9 +1544,9 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
                        D.ld, S.n_tiles, S.rows, S.ctr, S.tile_cnt, S.cand, S.cap, S.runs, S.n_chunks);
     hipLaunchKernelGGL(k_topk_sel_top, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, S.cand, S.cap, D.k,
                        S.sel_hist);
-    hipLaunchKernelGGL(k_topk_sel_collect, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap, D.k,
-                       S.sel_hist, S.play);
-    hipLaunchKernelGGL(k_topk_sel_finish, dim3(M), dim3(1024), 0, st, S.rows, S.cap, D.k, S.sel_hist, S.play,
+    hipLaunchKernelGGL(k_topk_sel_collect, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, S.cand, S.cap,
+                       D.k, S.sel_hist, S.play);
+    hipLaunchKernelGGL(k_topk_sel_finish, dim3(M), dim3(1024), 0, st, S.rows, S.ctr, S.cap, D.k, S.sel_hist, S.play,
                        S.fb_hist);
     for (int pass = 0; pass < kSelectPasses; ++pass)
         hipLaunchKernelGGL(k_topk_fb_hist, dim3(kFbBlocks), dim3(kBlock), 0, st, pass, G, E, eta, D.d, D.ld, D.M, D.k,
