@@ -299,7 +299,8 @@ constexpr int kPassTilesPerBlock = kPassTilesPerWave * (kBlock / 64);
 __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                       const TopkRow *__restrict__ rows, uint32_t *__restrict__ ctr,
-                                                      uint32_t *__restrict__ tile_cnt, uint2 *__restrict__ cand,
+                                                      uint32_t *__restrict__ tile_cnt, uint32_t *__restrict__ ckey,
+                                                      uint32_t *__restrict__ cidx,
                                                       int64_t cap, uint2 *__restrict__ runs, int64_t n_chunks) {
     constexpr uint32_t kStage = 256;  // staged candidates per wave
     constexpr int kWaves = kBlock / 64;
@@ -312,7 +313,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     const float *g = G + static_cast<int64_t>(m) * ld;
     const float *e = E + static_cast<int64_t>(m) * ld;
     const uint32_t span = hi - lo;
-    uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    uint32_t *krow = ckey + static_cast<int64_t>(m) * cap;
+    uint32_t *irow = cidx + static_cast<int64_t>(m) * cap;
     uint2 *stage = buf[wave];
     const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kPassTilesPerBlock + kPassTilesPerWave * wave;
     uint32_t my_cnt = 0;  // lane j < 16: above-band count of tile t0 + j
@@ -387,7 +389,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
                     for (int k = 0; k < 4; ++k) {
                         if ((cb[k] >> lane) & 1u) {
                             const int64_t j = static_cast<int64_t>(sbase) + pre;
-                            if (j < cap) crow[cap - 1 - j] = make_uint2(keys[k], static_cast<uint32_t>(i0 + k));
+                            if (j < cap) {
+                                krow[cap - 1 - j] = keys[k];
+                                irow[cap - 1 - j] = static_cast<uint32_t>(i0 + k);
+                            }
                             ++pre;
                         }
                     }
@@ -423,7 +428,11 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
     for (int w = 0; w < wave; ++w) off += wave_ns[w];
     for (uint32_t j = lane; j < ns; j += 64) {
         const int64_t pos = static_cast<int64_t>(off) + j;
-        if (pos < cap) crow[pos] = stage[j];
+        if (pos < cap) {
+            const uint2 c = stage[j];
+            krow[pos] = c.x;
+            irow[pos] = c.y;
+        }
     }
 }
 
@@ -437,10 +446,12 @@ __device__ __forceinline__ bool sel_ok(const TopkRow &r, int64_t k, int64_t cap)
     return n_listed(r) <= static_cast<uint64_t>(cap) && r.n_above < static_cast<uint64_t>(k) &&
            static_cast<uint64_t>(k) - r.n_above <= n_listed(r);
 }
-// Candidate j of a row's list: the runs [0, n_cand), then the spills stored
-// from the top down.
-__device__ __forceinline__ uint2 cand_at(const uint2 *__restrict__ crow, uint64_t j, uint32_t n_cand, int64_t cap) {
-    return crow[j < n_cand ? j : static_cast<uint64_t>(cap) - 1 - (j - n_cand)];
+// The place of candidate j in a row's list: the runs [0, n_cand), then the
+// spills stored from the top down.  The list is two planes of the row's
+// capacity, keys and indices, so that a search that needs only the keys
+// reads half the bytes.
+__device__ __forceinline__ uint64_t cand_pos(uint64_t j, uint32_t n_cand, int64_t cap) {
+    return j < n_cand ? j : static_cast<uint64_t>(cap) - 1 - (j - n_cand);
 }
 
 // The search over the candidates: the first digit of key - lo (its top 11
@@ -485,7 +496,7 @@ constexpr int kSelU = 8;  // candidates in flight per thread
 
 // The first key digit's histogram (kSelBlocks workgroups per row).
 __global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ rows, const uint32_t *__restrict__ ctr,
-                                                         const uint2 *__restrict__ cand, int64_t cap, int64_t k,
+                                                         const uint32_t *__restrict__ ckey, int64_t cap, int64_t k,
                                                          uint32_t *__restrict__ sel_hist) {
     __shared__ uint32_t h[kDigitBins];
     const int m = blockIdx.y;
@@ -507,7 +518,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ r
     const int nb = 1 << wbits;
     for (int b = threadIdx.x; b < nb; b += kBlock) h[b] = 0u;
     __syncthreads();
-    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    const uint32_t *krow = ckey + static_cast<int64_t>(m) * cap;
     const uint64_t n = n_listed(r);
     const uint64_t per = (n + kSelBlocks - 1) / kSelBlocks;
     const uint64_t j_lo = per * blockIdx.x, j_hi = j_lo + per < n ? j_lo + per : n;
@@ -516,7 +527,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ r
 #pragma unroll
         for (int u = 0; u < kSelU; ++u) {
             const uint64_t j = j0 + static_cast<uint64_t>(kBlock) * u;
-            keys[u] = j < j_hi ? cand_at(crow, j, r.n_cand, cap).x : 0u;
+            keys[u] = j < j_hi ? krow[cand_pos(j, r.n_cand, cap)] : 0u;
         }
 #pragma unroll
         for (int u = 0; u < kSelU; ++u)
@@ -532,7 +543,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ r
 // row; one atomic per wave and round).
 __global__ __launch_bounds__(kBlock) void k_topk_sel_collect(const TopkRow *__restrict__ rows,
                                                              uint32_t *__restrict__ ctr,
-                                                             const uint2 *__restrict__ cand, int64_t cap, int64_t k,
+                                                             const uint32_t *__restrict__ ckey,
+                                                             const uint32_t *__restrict__ cidx, int64_t cap, int64_t k,
                                                              const uint32_t *__restrict__ sel_hist,
                                                              uint2 *__restrict__ play) {
     __shared__ TopState st;
@@ -546,7 +558,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_collect(const TopkRow *__re
     __syncthreads();
     const TopState s = st;
     const int lane = threadIdx.x & 63;
-    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    const uint32_t *krow = ckey + static_cast<int64_t>(m) * cap;
+    const uint32_t *irow = cidx + static_cast<int64_t>(m) * cap;
     uint2 *prow = play + static_cast<int64_t>(m) * cap;
     const uint64_t n = n_listed(r);
     const uint64_t per = (n + kSelBlocks - 1) / kSelBlocks;
@@ -555,18 +568,18 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_collect(const TopkRow *__re
     // examined; every thread of the workgroup in each round), one atomic per
     // wave and round
     for (uint64_t jb = j_lo; jb < j_hi; jb += static_cast<uint64_t>(kBlock) * kSelU) {
-        uint2 cs[kSelU];
+        uint32_t ks[kSelU];  // keys; a candidate's index is read only when it is listed
         uint64_t mask[kSelU];
         uint32_t tot = 0;
 #pragma unroll
         for (int u = 0; u < kSelU; ++u) {
             const uint64_t j = jb + static_cast<uint64_t>(kBlock) * u + threadIdx.x;
-            cs[u] = j < j_hi ? cand_at(crow, j, r.n_cand, cap) : make_uint2(0u, 0u);
+            ks[u] = j < j_hi ? krow[cand_pos(j, r.n_cand, cap)] : 0u;
         }
 #pragma unroll
         for (int u = 0; u < kSelU; ++u) {
             const uint64_t j = jb + static_cast<uint64_t>(kBlock) * u + threadIdx.x;
-            const uint32_t rel = cs[u].x - r.lo;
+            const uint32_t rel = ks[u] - r.lo;
             mask[u] = __ballot(j < j_hi && (s.top >= 32 || (rel >> s.top) == (s.kp >> s.top)));
             tot += __popcll(mask[u]);
         }
@@ -580,7 +593,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_collect(const TopkRow *__re
                     const uint32_t at = base + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask[u] >> 32),
                                                                          __builtin_amdgcn_mbcnt_lo(
                                                                              static_cast<uint32_t>(mask[u]), 0u));
-                    if (at < cap) prow[at] = cs[u];
+                    const uint64_t j = jb + static_cast<uint64_t>(kBlock) * u + threadIdx.x;
+                    if (at < cap) prow[at] = make_uint2(ks[u], irow[cand_pos(j, r.n_cand, cap)]);
                 }
                 base += static_cast<uint32_t>(__popcll(mask[u]));
             }
@@ -825,17 +839,19 @@ __global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restr
 constexpr int kSpillBlocks = 16;  // workgroups per row
 
 __global__ __launch_bounds__(kBlock) void k_topk_spill_count(const TopkRow *__restrict__ rows,
-                                                             const uint2 *__restrict__ cand, int64_t cap,
+                                                             const uint32_t *__restrict__ ckey,
+                                                             const uint32_t *__restrict__ cidx, int64_t cap,
                                                              uint32_t *__restrict__ tile_cnt, int64_t n_tiles) {
     const int m = blockIdx.y;
     const TopkRow r = rows[m];
     if (r.fallback || r.n_spill == 0) return;
-    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    const uint32_t *krow = ckey + static_cast<int64_t>(m) * cap;
+    const uint32_t *irow = cidx + static_cast<int64_t>(m) * cap;
     uint32_t *trow = tile_cnt + static_cast<int64_t>(m) * n_tiles;
     const int64_t n = r.n_spill;  // at most cap - n_cand (the search decided)
     for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n;
          j += static_cast<int64_t>(gridDim.x) * kBlock) {
-        const uint2 c = crow[cap - 1 - j];
+        const uint2 c = make_uint2(krow[cap - 1 - j], irow[cap - 1 - j]);
         if (c.x > r.T || (c.x == r.T && c.y <= r.I)) atomicAdd(&trow[c.y / kTopkTile], 1u);
     }
 }
@@ -850,7 +866,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_spill_count(const TopkRow *__re
 constexpr int kScanChunksPerWave = 4;
 
 __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__restrict__ rows,
-                                                            const uint2 *__restrict__ cand, int64_t cap,
+                                                            const uint32_t *__restrict__ ckey,
+                                                            const uint32_t *__restrict__ cidx, int64_t cap,
                                                             const uint2 *__restrict__ runs,
                                                             const uint32_t *__restrict__ tile_cnt,
                                                             uint32_t *__restrict__ tile_off,
@@ -872,7 +889,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__res
         cnt[q] = (c < n_chunks && t < n_tiles) ? tile_cnt[static_cast<int64_t>(m) * n_tiles + t] : 0u;
         run[q] = c < n_chunks ? runs[static_cast<int64_t>(m) * n_chunks + c] : make_uint2(0u, 0u);
     }
-    const uint2 *crow = cand + static_cast<int64_t>(m) * cap;
+    const uint32_t *krow = ckey + static_cast<int64_t>(m) * cap;
+    const uint32_t *irow = cidx + static_cast<int64_t>(m) * cap;
 #pragma unroll
     for (int q = 0; q < kScanChunksPerWave; ++q) {
         const int64_t c = c0 + q;
@@ -896,7 +914,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__res
                 for (int u = 0; u < kRunU; ++u) {
                     const uint32_t j = j0 + 64 * u;
                     const int64_t pos = static_cast<int64_t>(run[q].x) + j;
-                    cd[u] = (j < run[q].y && pos < cap) ? crow[pos] : make_uint2(0u, 0xFFFFFFFFu);
+                    cd[u] = (j < run[q].y && pos < cap) ? make_uint2(krow[pos], irow[pos]) : make_uint2(0u, 0xFFFFFFFFu);
                 }
 #pragma unroll
                 for (int u = 0; u < kRunU; ++u) {
@@ -1534,6 +1552,9 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     const TopkScratch &S = P.topk;
     const dqgan_desc &D = P.desc;
     const unsigned M = static_cast<unsigned>(D.M);
+    // the candidate lists: a key plane [M][cap], then an index plane [M][cap]
+    uint32_t *ckey = reinterpret_cast<uint32_t *>(S.cand);
+    uint32_t *cidx = ckey + static_cast<int64_t>(D.M) * S.cap;
     const int64_t sb = (S.n_sample_chunks + kSampleThreads / 64 - 1) / (kSampleThreads / 64);
     hipLaunchKernelGGL(k_topk_sample, dim3(static_cast<unsigned>(sb < kSampleBlocks ? sb : kSampleBlocks), M),
                        dim3(kSampleThreads), 0, st,
@@ -1541,11 +1562,11 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
     hipLaunchKernelGGL(k_topk_band, dim3(M), dim3(1024), 0, st, S.hist, S.sel_hist, S.rows, S.ctr, S.n_samples, D.d,
                        D.k);
     hipLaunchKernelGGL(k_topk_pass, dim3(static_cast<unsigned>(S.n_chunks), M), dim3(kBlock), 0, st, G, E, eta, D.d,
-                       D.ld, S.n_tiles, S.rows, S.ctr, S.tile_cnt, S.cand, S.cap, S.runs, S.n_chunks);
-    hipLaunchKernelGGL(k_topk_sel_top, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, S.cand, S.cap, D.k,
+                       D.ld, S.n_tiles, S.rows, S.ctr, S.tile_cnt, ckey, cidx, S.cap, S.runs, S.n_chunks);
+    hipLaunchKernelGGL(k_topk_sel_top, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, ckey, S.cap, D.k,
                        S.sel_hist);
-    hipLaunchKernelGGL(k_topk_sel_collect, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, S.cand, S.cap,
-                       D.k, S.sel_hist, S.play);
+    hipLaunchKernelGGL(k_topk_sel_collect, dim3(kSelBlocks, M), dim3(kBlock), 0, st, S.rows, S.ctr, ckey, cidx,
+                       S.cap, D.k, S.sel_hist, S.play);
     hipLaunchKernelGGL(k_topk_sel_finish, dim3(M), dim3(1024), 0, st, S.rows, S.ctr, S.cap, D.k, S.sel_hist, S.play,
                        S.fb_hist);
     for (int pass = 0; pass < kSelectPasses; ++pass)
@@ -1553,12 +1574,12 @@ hipError_t launch_topk_select(const dqgan_plan_s &P, float eta, const float *G, 
                            S.rows, S.fb_hist);
     hipLaunchKernelGGL(k_topk_fb_recount, dim3(256), dim3(kBlock), 0, st, G, E, eta, D.d, D.ld, S.n_tiles, D.M, D.k,
                        S.rows, S.fb_hist, S.tile_cnt);
-    hipLaunchKernelGGL(k_topk_spill_count, dim3(kSpillBlocks, M), dim3(kBlock), 0, st, S.rows, S.cand, S.cap,
+    hipLaunchKernelGGL(k_topk_spill_count, dim3(kSpillBlocks, M), dim3(kBlock), 0, st, S.rows, ckey, cidx, S.cap,
                        S.tile_cnt, S.n_tiles);
     const int64_t scan_per_block = (kBlock / 64) * kScanChunksPerWave;
     hipLaunchKernelGGL(k_topk_count_scan, dim3(static_cast<unsigned>((S.n_chunks + scan_per_block - 1) / scan_per_block), M),
                        dim3(kBlock), 0, st,
-                       S.rows, S.cand,
+                       S.rows, ckey, cidx,
                        S.cap, S.runs, S.tile_cnt, S.tile_off, S.chunk_sum, S.n_tiles, S.n_chunks);
     hipLaunchKernelGGL(k_topk_chunk_scan, dim3(M), dim3(1024), 0, st, S.rows, S.chunk_sum, S.chunk_off, S.n_chunks);
     return hipGetLastError();
