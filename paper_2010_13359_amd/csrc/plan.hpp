@@ -86,8 +86,8 @@ struct TopkScratch {
     uint2 *cand = nullptr;          // [M][cap] (key, index) candidates: runs from the bottom, spills from the top
     int64_t cap = 0;
     uint2 *runs = nullptr;          // [M][n_chunks] (first position, count) of each full-pass workgroup's candidates
-    uint32_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per 256-element tile
-    uint32_t *tile_off = nullptr;   // [M][n_tiles] selected elements before the tile within its chunk
+    uint16_t *tile_cnt = nullptr;   // [M][n_tiles] selected elements per 256-element tile (at most 256)
+    uint16_t *tile_off = nullptr;   // [M][n_tiles] selected elements before the tile within its chunk (< 2^14)
     uint32_t *chunk_sum = nullptr;  // [M][n_chunks] selected elements per chunk of kTopkChunkTiles tiles
     uint32_t *chunk_off = nullptr;  // [M][n_chunks] exclusive prefix of chunk_sum
     uint32_t *agg_start = nullptr;  // [n_agg_tiles + 1][M] first message entry per server-average tile
@@ -102,7 +102,7 @@ struct TopkScratch {
 // first output position, tile_off + chunk_off of its chunk.
 struct TopkArgs {
     const TopkRow *rows;
-    const uint32_t *tile_off;
+    const uint16_t *tile_off;
     const uint32_t *chunk_off;
     int64_t n_tiles;
     int64_t n_chunks;

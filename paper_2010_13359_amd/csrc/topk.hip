@@ -281,8 +281,9 @@ __global__ __launch_bounds__(1024) void k_topk_band(uint32_t *__restrict__ hist,
 // tiles of one row; wave w owns 16 consecutive tiles of them, four per round
 // (the round's eight loads issued before its first tile is examined).  Lane j
 // of a wave keeps the count of the wave's j-th tile, and the wave writes its
-// 16 counts with one 64-byte store at the end: over 64 rows of 10^8 elements
-// a 4-byte count store per tile held the pass 8 % above its loads alone.
+// 16 counts (16-bit) with one 32-byte store at the end: over 64 rows of
+// 10^8 elements a 4-byte count store per tile held the pass 8 % above its
+// loads alone.
 // Candidates are staged in the wave's quarter of an LDS buffer with a
 // wave-uniform count; at the end the workgroup adds its above-band total
 // (the sum of its tile counts) to the row's counters and writes its
@@ -299,7 +300,7 @@ constexpr int kPassTilesPerBlock = kPassTilesPerWave * (kBlock / 64);
 __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ G, const float *__restrict__ E,
                                                       float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                       const TopkRow *__restrict__ rows, uint32_t *__restrict__ ctr,
-                                                      uint32_t *__restrict__ tile_cnt, uint32_t *__restrict__ ckey,
+                                                      uint16_t *__restrict__ tile_cnt, uint32_t *__restrict__ ckey,
                                                       uint32_t *__restrict__ cidx,
                                                       int64_t cap, uint2 *__restrict__ runs, int64_t n_chunks) {
     constexpr uint32_t kStage = 256;  // staged candidates per wave
@@ -401,7 +402,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_pass(const float *__restrict__ 
         }
     }
     // the wave's 16 tile counts: lanes 0..15, one contiguous store
-    if (lane < kPassTilesPerWave && t0 + lane < n_tiles) tile_cnt[static_cast<int64_t>(m) * n_tiles + t0 + lane] = my_cnt;
+    if (lane < kPassTilesPerWave && t0 + lane < n_tiles)
+        tile_cnt[static_cast<int64_t>(m) * n_tiles + t0 + lane] = static_cast<uint16_t>(my_cnt);
     // keys above the band in the wave's tiles: the sum of its 16 tile counts
     uint32_t nab = my_cnt;
 #pragma unroll
@@ -794,7 +796,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restr
                                                             float eta, int64_t d, int64_t ld, int64_t n_tiles,
                                                             int32_t M, int64_t k, TopkRow *__restrict__ rows,
                                                             const uint32_t *__restrict__ fb_hist,
-                                                            uint32_t *__restrict__ tile_cnt) {
+                                                            uint16_t *__restrict__ tile_cnt) {
     __shared__ FbState st;
     __shared__ int fb_rows[kMaxRows];
     __shared__ int n_fb;
@@ -827,7 +829,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_fb_recount(const float *__restr
                 const bool sel = i < d && (key > s.T || (key == s.T && static_cast<uint32_t>(i) <= s.I));
                 n += __popcll(__ballot(sel));
             }
-            if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = n;
+            if (lane == 0) tile_cnt[static_cast<int64_t>(m) * n_tiles + tile] = static_cast<uint16_t>(n);
         }
         __syncthreads();  // st is reused for the next row
     }
@@ -841,18 +843,24 @@ constexpr int kSpillBlocks = 16;  // workgroups per row
 __global__ __launch_bounds__(kBlock) void k_topk_spill_count(const TopkRow *__restrict__ rows,
                                                              const uint32_t *__restrict__ ckey,
                                                              const uint32_t *__restrict__ cidx, int64_t cap,
-                                                             uint32_t *__restrict__ tile_cnt, int64_t n_tiles) {
+                                                             uint16_t *__restrict__ tile_cnt, int64_t n_tiles) {
     const int m = blockIdx.y;
     const TopkRow r = rows[m];
     if (r.fallback || r.n_spill == 0) return;
     const uint32_t *krow = ckey + static_cast<int64_t>(m) * cap;
     const uint32_t *irow = cidx + static_cast<int64_t>(m) * cap;
-    uint32_t *trow = tile_cnt + static_cast<int64_t>(m) * n_tiles;
+    // 32-bit atomics on the word holding the tile's 16-bit count (n_tiles is
+    // a multiple of 4, so a row's counts start on a word; a count stays at
+    // most 256 and never carries into its neighbour)
+    uint32_t *trow = reinterpret_cast<uint32_t *>(tile_cnt + static_cast<int64_t>(m) * n_tiles);
     const int64_t n = r.n_spill;  // at most cap - n_cand (the search decided)
     for (int64_t j = static_cast<int64_t>(blockIdx.x) * kBlock + threadIdx.x; j < n;
          j += static_cast<int64_t>(gridDim.x) * kBlock) {
         const uint2 c = make_uint2(krow[cap - 1 - j], irow[cap - 1 - j]);
-        if (c.x > r.T || (c.x == r.T && c.y <= r.I)) atomicAdd(&trow[c.y / kTopkTile], 1u);
+        if (c.x > r.T || (c.x == r.T && c.y <= r.I)) {
+            const uint32_t tile = c.y / kTopkTile;
+            atomicAdd(&trow[tile >> 1], 1u << (16u * (tile & 1u)));
+        }
     }
 }
 
@@ -869,8 +877,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__res
                                                             const uint32_t *__restrict__ ckey,
                                                             const uint32_t *__restrict__ cidx, int64_t cap,
                                                             const uint2 *__restrict__ runs,
-                                                            const uint32_t *__restrict__ tile_cnt,
-                                                            uint32_t *__restrict__ tile_off,
+                                                            const uint16_t *__restrict__ tile_cnt,
+                                                            uint16_t *__restrict__ tile_off,
                                                             uint32_t *__restrict__ chunk_sum, int64_t n_tiles,
                                                             int64_t n_chunks) {
     __shared__ uint32_t sel_all[kBlock / 64][kTopkChunkTiles];
@@ -936,7 +944,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__res
             const uint32_t v = __shfl_up(incl, o);
             if (lane >= o) incl += v;
         }
-        if (t < n_tiles) tile_off[static_cast<int64_t>(m) * n_tiles + t] = incl - n_here;
+        if (t < n_tiles) tile_off[static_cast<int64_t>(m) * n_tiles + t] = static_cast<uint16_t>(incl - n_here);
         if (lane == 63) chunk_sum[static_cast<int64_t>(m) * n_chunks + c] = incl;
     }
 }
@@ -1515,9 +1523,9 @@ hipError_t topk_alloc(dqgan_plan_s &P) {
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.runs), M * static_cast<size_t>(S.n_chunks) * sizeof(uint2));
     if (e == hipSuccess)
-        e = hipMalloc(reinterpret_cast<void **>(&S.tile_cnt), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
+        e = hipMalloc(reinterpret_cast<void **>(&S.tile_cnt), M * static_cast<size_t>(S.n_tiles) * sizeof(uint16_t));
     if (e == hipSuccess)
-        e = hipMalloc(reinterpret_cast<void **>(&S.tile_off), M * static_cast<size_t>(S.n_tiles) * sizeof(uint32_t));
+        e = hipMalloc(reinterpret_cast<void **>(&S.tile_off), M * static_cast<size_t>(S.n_tiles) * sizeof(uint16_t));
     if (e == hipSuccess)
         e = hipMalloc(reinterpret_cast<void **>(&S.chunk_sum), M * static_cast<size_t>(S.n_chunks) * sizeof(uint32_t));
     if (e == hipSuccess)
