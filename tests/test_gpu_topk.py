@@ -2,8 +2,9 @@
 through the C ABI, against the oracle on the same inputs.  Indices and
 values of the message, residuals, the average and the OMD outputs must be
 identical.  Shapes cover the sampled-band path (Gaussian and Laplace data),
-the full-row fallback (heavy ties, all-zero rows, k = d) and every launch
-shape of the apply pass (up to 300 workers)."""
+candidates spilled past a wave's staging (a dense band), the full-row
+fallback (heavy ties, all-zero rows, k = d) and every launch shape of the
+apply pass (up to 300 workers)."""
 import numpy as np
 import pytest
 
@@ -40,6 +41,12 @@ def _case(name):
         # 700 equal large values outside the sampled chunks: more than k keys
         # lie above the band, so the full-row search decides
         return custom(d=200000, M=2, kind="topk", k=500, eta=1e-2, seed=32), "cluster"
+    if name == "m2_dense_band":
+        # a block of 10000 consecutive values just below the 15000 largest:
+        # the k-th key lies in it, so the band holds the whole block and the
+        # waves over it overflow their staging (spilled candidates, counted
+        # per tile by the spill count), while the list stays below capacity
+        return custom(d=300000, M=2, kind="topk", k=20000, eta=1.0, seed=38), "band"
     if name == "m16_d1000000_k10000":
         return custom(d=1000000, M=16, kind="topk", k=10000, eta=1e-3, seed=29), None
     # more than 64 workers: 16 waves x 8 rows (65..128), then one lane
@@ -58,7 +65,8 @@ def _case(name):
 
 
 NAMES = ["m4_d5000_k50", "m8_d200000_k2000", "m5_d3001_k7", "m64_d300000_k3000", "m3_d1_k1", "m2_d4096_kd",
-         "m4_ties", "m4_ties_big", "m4_zero_rows", "m2_hidden_cluster", "m16_d1000000_k10000", "m65_d20000_k200",
+         "m4_ties", "m4_ties_big", "m4_zero_rows", "m2_hidden_cluster", "m2_dense_band", "m16_d1000000_k10000",
+         "m65_d20000_k200",
          "m128_d9000_k90", "m130_d7001_k70", "m300_d3000_k3000", "m1024_d2500_k25"]
 
 
@@ -74,6 +82,15 @@ def _inputs(name):
     if special == "cluster":
         G[:, 1000:1700] = 100.0
         G[1, 1200:1300] = -100.0
+    if special == "band":
+        rng = np.random.default_rng(5)
+        G[:, :w.d] = (1e-3 * rng.standard_normal((w.M, w.d))).astype(np.float32)
+        E[:, :w.d] = 0.0
+        for m in range(w.M):
+            big = rng.choice(np.setdiff1d(np.arange(w.d), np.arange(100000, 110000)), 15000, replace=False)
+            G[m, big] = (10.0 + rng.standard_normal(15000)).astype(np.float32)
+            sign = 1.0 if m == 0 else -1.0
+            G[m, 100000:110000] = (sign * (1.0 + 1e-4 * rng.standard_normal(10000))).astype(np.float32)
     if special == "zeros":
         G[1, :] = 0.0
         E[1, :] = 0.0
