@@ -63,3 +63,52 @@ def test_uniforms_statistics(oracle_mod):
     assert abs(c) < 6 / np.sqrt(n)
     # 24-bit grid
     assert np.all(u * (1 << 24) == np.floor(u * (1 << 24)))
+
+
+_ROCRAND_PROBE = r"""
+#include <cstdio>
+#include <rocrand/rocrand_kernel.h>
+// rocRAND's Philox4x32-10 block function (host-callable), made public
+struct Engine : rocrand_device::philox4x32_10_engine {
+    using rocrand_device::philox4x32_10_engine::ten_rounds;
+};
+int main() {
+    Engine eng;
+    unsigned c0, c1, c2, c3, k0, k1;
+    while (std::scanf("%u %u %u %u %u %u", &c0, &c1, &c2, &c3, &k0, &k1) == 6) {
+        uint4 c; c.x = c0; c.y = c1; c.z = c2; c.w = c3;
+        uint2 k; k.x = k0; k.y = k1;
+        const uint4 r = eng.ten_rounds(c, k);
+        std::printf("%u %u %u %u\n", r.x, r.y, r.z, r.w);
+    }
+    return 0;
+}
+"""
+
+
+def test_c_oracle_matches_rocrand_philox4x32(oracle_mod, tmp_path):
+    """The oracle's 32-bit instance against an implementation outside this
+    repository: rocRAND's Philox4x32-10 block function (its multipliers,
+    Weyl key increments and round order), run on the host."""
+    import os
+    import subprocess
+    import pytest
+    hipcc = "/opt/rocm/bin/hipcc"
+    if not (os.path.exists(hipcc) and os.path.exists("/opt/rocm/include/rocrand/rocrand_philox4x32_10.h")):
+        pytest.skip("hipcc or rocRAND headers not installed")
+    src = tmp_path / "rocrand_philox.cpp"
+    exe = tmp_path / "rocrand_philox"
+    src.write_text(_ROCRAND_PROBE)
+    subprocess.run([hipcc, "--offload-arch=gfx950", "-O1", "-o", str(exe), str(src)], check=True,
+                   capture_output=True, timeout=300)
+    rng = random.Random(4321)
+    cases = [([rng.getrandbits(32) for _ in range(4)], [rng.getrandbits(32) for _ in range(2)]) for _ in range(3000)]
+    for c in ([0, 0, 0, 0], [0xFFFFFFFF] * 4, [1, 0, 0, 0], [0, 0, 0, 1]):
+        for k in ([0, 0], [0xFFFFFFFF, 0xFFFFFFFF], [0x9E3779B9, 0]):
+            cases.append((c, k))
+    stdin = "".join("%d %d %d %d %d %d\n" % (*c, *k) for c, k in cases)
+    out = subprocess.run([str(exe)], input=stdin, capture_output=True, text=True, check=True, timeout=120).stdout
+    got = [list(map(int, line.split())) for line in out.strip().splitlines()]
+    assert len(got) == len(cases)
+    for (c, k), r in zip(cases, got):
+        assert oracle_mod.philox4x32_10(c, k) == r, (c, k)
