@@ -507,7 +507,9 @@ __global__ __launch_bounds__(kBlock) void k_topk_sel_top(TopkRow *__restrict__ r
     r.n_cand = c[kCtrCand];
     r.n_above = c[kCtrAbove];
     r.n_spill = c[kCtrSpill];
-    // the later kernels read the counters from the row record
+    // the later kernels read the counters from the row record (the other
+    // workgroups of this launch may read the record meanwhile: they take
+    // the counters from ctr, and the rest of the record does not change)
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         rows[m].n_cand = r.n_cand;
         rows[m].n_above = r.n_above;
