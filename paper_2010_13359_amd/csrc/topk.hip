@@ -1033,10 +1033,12 @@ __device__ __forceinline__ int agg_col(int t, int i) { return (i < 4 ? 0 : kAggH
 // in coalesced rounds (round u: chunk u * 64 + lane), all loaded before the
 // first is examined; a chunk's entries outside the row are not the row's.
 // A round whose last entry lies in the tile of the entry before the round
-// starts nothing (sorted lists) and is passed over.  Otherwise an entry that
-// starts one tile writes it; where one starts several (a run of empty
-// tiles) the wave writes them together, lane q taking the q-th.
+// starts nothing (sorted lists) and is passed over.  Otherwise each lane
+// writes the starts of its own entries (an entry after a run of empty tiles
+// starts all of them), except a lane with more than kStartsLongRun to write,
+// whose starts the whole wave writes.
 constexpr int kStartsLoads = 4;
+constexpr int kStartsLongRun = 8;  // more starts than this per lane and round: written by the wave
 
 __device__ __forceinline__ uint32_t u4_at(const uint4 &v, int i) {
     return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w;
@@ -1049,8 +1051,9 @@ __global__ __launch_bounds__(kBlock) void k_topk_agg_starts(const uint32_t *__re
     // (b % 8) takes M / 8 consecutive rows: a tile's M starts are written
     // close in time, each contiguous eighth of them from one L2, which merges
     // the 4-byte stores before they reach HBM.
-    const int64_t b = blockIdx.x;
-    const int seg = static_cast<int>(b / M), t = static_cast<int>(b % M);
+    const uint32_t b = blockIdx.x, um = static_cast<uint32_t>(M);
+    const uint32_t useg = b / um;
+    const int seg = static_cast<int>(useg), t = static_cast<int>(b - useg * um);
     const int m = M % 8 == 0 ? (t % 8) * (M / 8) + t / 8 : t;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int64_t row0 = static_cast<int64_t>(m) * k;  // flat index of the row's first entry
@@ -1072,56 +1075,54 @@ __global__ __launch_bounds__(kBlock) void k_topk_agg_starts(const uint32_t *__re
     };
     const int64_t j_wave = 4 * (c_first + cw) - row0;  // the wave's first entry (row-relative)
     int t_before = j_wave - 1 >= 0 ? tile_of(j_wave - 1, idx[row0 + j_wave - 1]) : -1;
+    // every entry the wave loaded lies in the row (all waves but the first
+    // and last of a row): the tile is the index's alone
+    const bool inside = j_wave >= 0 && j_wave + 4 * 64 * kStartsLoads <= k;
 #pragma unroll
     for (int u = 0; u < kStartsLoads; ++u) {
         const int64_t j0 = j_wave + 4 * (64 * u + lane);  // row-relative index of the chunk's entry 0
         int t[4];
+        if (inside) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) t[i] = tile_of(j0 + i, u4_at(v[u], i));
+            for (int i = 0; i < 4; ++i) t[i] = min(static_cast<int>(u4_at(v[u], i) / kAggTile), n_t);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) t[i] = tile_of(j0 + i, u4_at(v[u], i));
+        }
         const int t_round_last = __builtin_amdgcn_readlane(t[3], 63);
         if (t_round_last == t_before) continue;  // no entry of the round starts a tile
-        const int t_prev_lane = __shfl_up(t[3], 1);
+        // the tile of the previous lane's last entry (DPP shift right by one
+        // lane across the wave; lane 0 keeps t_before, the tile of the entry
+        // before the round)
         int n[4];
-        int tp = lane > 0 ? t_prev_lane : t_before;
-        bool many = false;
+        int tp = __builtin_amdgcn_update_dpp(t_before, t[3], 0x138, 0xF, 0xF, false);
+        int n_lane = 0;  // the tiles this lane's four entries start
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             n[i] = t[i] > tp ? t[i] - tp : 0;
-            many = many || n[i] > 1;
+            n_lane += n[i];
             tp = t[i] > tp ? t[i] : tp;
         }
         t_before = t_round_last;
-        if (__ballot(many) == 0) {
+        // Each lane writes the starts of its own entries, entry j0 + i those of
+        // tiles t[i] - n[i] + 1 .. t[i], except a lane that starts a long run
+        // of empty tiles: the wave writes that lane's starts together, 64 at a
+        // time, one such lane after the other.
+        const uint64_t lng = __ballot(n_lane > kStartsLongRun);
+        if (n_lane <= kStartsLongRun) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                if (n[i] == 1) start[static_cast<int64_t>(t[i]) * M + m] = static_cast<uint32_t>(j0 + i);
-            continue;
+                for (int q = 0; q < n[i]; ++q)
+                    start[static_cast<int64_t>(t[i] - q) * M + m] = static_cast<uint32_t>(j0 + i);
         }
-        // some entry starts several tiles: entry i of every lane in turn,
-        // the wave writing their starts together
+        for (uint64_t rest = lng; rest != 0; rest &= rest - 1) {
+            const int L = __builtin_ctzll(rest);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint32_t ni = static_cast<uint32_t>(n[i]);
-            uint32_t incl = ni;
-#pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const uint32_t x = __shfl_up(incl, o);
-                if (lane >= o) incl += x;
-            }
-            const uint32_t total = __shfl(incl, 63);
-            for (uint32_t q0 = 0; q0 < total; q0 += 64) {
-                const uint32_t q = q0 + lane;
-                int o = 0;  // the owner of start q: the number of lanes with incl <= q
-#pragma unroll
-                for (int sh = 32; sh > 0; sh >>= 1)
-                    if (static_cast<uint32_t>(__shfl(incl, o + sh - 1)) <= q) o += sh;
-                const uint32_t o_incl = __shfl(incl, o);
-                const int o_t = __shfl(t[i], o);
-                if (q < total) {
-                    const int64_t T = static_cast<int64_t>(o_t) - (o_incl - 1 - q);  // o's tiles end at o_t
-                    const int64_t j = j_wave + 4 * (64 * u + o) + i;
-                    start[T * M + m] = static_cast<uint32_t>(j);
-                }
+            for (int i = 0; i < 4; ++i) {
+                const int nl = __builtin_amdgcn_readlane(n[i], L);
+                const int tl = __builtin_amdgcn_readlane(t[i], L);
+                const uint32_t jl = static_cast<uint32_t>(j_wave + 4 * (64 * u + L) + i);
+                for (int q = lane; q < nl; q += 64) start[static_cast<int64_t>(tl - q) * M + m] = jl;
             }
         }
     }
