@@ -452,6 +452,21 @@ __device__ __forceinline__ bool sel_ok(const TopkRow &r, int64_t k, int64_t cap)
 // spills stored from the top down.  The list is two planes of the row's
 // capacity, keys and indices, so that a search that needs only the keys
 // reads half the bytes.
+// Inclusive prefix sum over the 64 lanes of a wave, all of them active, by
+// data-parallel-primitive moves: shifts by 1, 2, 4 and 8 lanes inside each
+// row of 16 lanes (a lane whose source lies before its row reads 0), then
+// the last lane of rows 0 and 2 added to rows 1 and 3, then the last lane of
+// row 1 added to rows 2 and 3.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+    x += __builtin_amdgcn_update_dpp(0u, x, 0x111, 0xF, 0xF, true);   // row_shr:1
+    x += __builtin_amdgcn_update_dpp(0u, x, 0x112, 0xF, 0xF, true);   // row_shr:2
+    x += __builtin_amdgcn_update_dpp(0u, x, 0x114, 0xF, 0xF, true);   // row_shr:4
+    x += __builtin_amdgcn_update_dpp(0u, x, 0x118, 0xF, 0xF, true);   // row_shr:8
+    x += __builtin_amdgcn_update_dpp(0u, x, 0x142, 0xA, 0xF, false);  // row_bcast:15, rows 1 and 3
+    x += __builtin_amdgcn_update_dpp(0u, x, 0x143, 0xC, 0xF, false);  // row_bcast:31, rows 2 and 3
+    return x;
+}
+
 __device__ __forceinline__ uint64_t cand_pos(uint64_t j, uint32_t n_cand, int64_t cap) {
     return j < n_cand ? j : static_cast<uint64_t>(cap) - 1 - (j - n_cand);
 }
@@ -940,12 +955,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_count_scan(const TopkRow *__res
             __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
             n_here += sel[lane];
         }
-        uint32_t incl = n_here;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t v = __shfl_up(incl, o);
-            if (lane >= o) incl += v;
-        }
+        const uint32_t incl = wave_incl_scan(n_here);
         if (t < n_tiles) tile_off[static_cast<int64_t>(m) * n_tiles + t] = static_cast<uint16_t>(incl - n_here);
         if (lane == 63) chunk_sum[static_cast<int64_t>(m) * n_chunks + c] = incl;
     }
@@ -1315,12 +1325,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
         const int64_t s0 = min(static_cast<int64_t>(s_raw), k);
         const int64_t e0 = min(static_cast<int64_t>(e_raw), k);
         const uint32_t rn = e0 > s0 ? static_cast<uint32_t>(min(e0 - s0, static_cast<int64_t>(kAggTile))) : 0u;
-        uint32_t incl = rn;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t x = __shfl_up(incl, o);
-            if (lane >= o) incl += x;
-        }
+        const uint32_t incl = wave_incl_scan(rn);
         const uint32_t total = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(incl), 63));
         if (total == 0u) {
 #pragma unroll
@@ -1332,12 +1337,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                                               static_cast<unsigned long long>(s0);
                 const unsigned long long c0 = G0 >> 2;
                 const uint32_t nc = rn ? static_cast<uint32_t>(((G0 + rn + 3) >> 2) - c0) : 0u;
-                uint32_t cincl = nc;
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) {
-                    const uint32_t y = __shfl_up(cincl, o);
-                    if (lane >= o) cincl += y;
-                }
+                const uint32_t cincl = wave_incl_scan(nc);
                 R.woff[lane] = incl - rn;
                 R.ch_c0[lane] = c0;
                 R.ch_off[lane] = cincl - nc;
@@ -1381,12 +1381,7 @@ __global__ __launch_bounds__(kBlock, 4) void k_topk_agg_tiles(const float *__res
                     cnt[i] = static_cast<uint32_t>(__popcll(S.s.mask[agg_col(tid, i)]));
                     mine += cnt[i];
                 }
-                uint32_t incl = mine;
-#pragma unroll
-                for (int o = 1; o < 64; o <<= 1) {
-                    const uint32_t x = __shfl_up(incl, o);
-                    if (lane >= o) incl += x;
-                }
+                const uint32_t incl = wave_incl_scan(mine);
                 if (lane == 63) wsum[wave] = incl;
                 lds_barrier();
                 uint32_t pos = incl - mine;
