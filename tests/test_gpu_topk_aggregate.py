@@ -14,7 +14,9 @@ columns: every worker sends -0 (the average is -0), every worker but one
 sends -0 (+0), and one worker alone sends -0 (+0).  The full-size check
 compares the server average of the 64 x 1e6 top-k messages of the largest
 workload with the fused step's, which the parity tests of that workload tie
-to the oracle.  Two checks cover messages outside the format: sorted lists
+to the oracle.  Lists with runs of empty tiles of every length between a
+worker's entries check the start of every tile.  Two checks cover messages
+outside the format: sorted lists
 ending in indices at or beyond d (skipped, so the average is the oracle's
 over the rest), and unsorted, repeated and out-of-range indices (undefined
 values, but the calls complete, their outputs are finite and the same plan
@@ -129,6 +131,48 @@ def test_topk_average_matches_oracle(name):
     assert np.signbit(got[ALL_NEG0]) and got[ALL_NEG0] == 0
     if M >= 3:
         assert not np.signbit(got[ALL_BUT_ONE_NEG0]) and not np.signbit(got[ONE_NEG0])
+
+
+def _gap_messages(M, k, seed):
+    """Sorted lists whose consecutive entries lie 0, 1, 2, 7, 8, 9, 10, 40 or
+    120 column tiles (2048 columns) apart, at most four in one tile: the
+    tiles between two entries have no entry of that worker, and a run of
+    four entries starts anything from none to hundreds of tiles."""
+    rng = np.random.default_rng(seed)
+    gaps = np.array([0, 0, 1, 2, 7, 8, 9, 10, 40, 120])
+    cols = []
+    for m in range(M):
+        g = rng.choice(gaps, size=k)
+        g[0] = rng.integers(0, 3)
+        run = 0
+        for j in range(1, k):  # at most four entries per tile
+            run = run + 1 if g[j] == 0 else 0
+            if run == 4:
+                g[j], run = 1, 0
+        T = np.cumsum(g)
+        off = np.empty(k, np.int64)
+        for t in np.unique(T):
+            sel = np.flatnonzero(T == t)
+            off[sel] = np.sort(rng.choice(2048, size=sel.size, replace=False))
+        cols.append(T * 2048 + off)
+    d = int(max(c[-1] for c in cols)) + 1 + int(rng.integers(0, 5000))
+    idx = np.stack(cols).astype(np.uint32)
+    val = (rng.standard_normal((M, k)) * 10.0 ** rng.uniform(-8, 8, (M, k))).astype(np.float32)
+    return d, idx, val
+
+
+@pytest.mark.parametrize("M,k", [(6, 300), (66, 40)])
+def test_topk_average_runs_of_empty_tiles(M, k):
+    """Runs of empty tiles of every length between a worker's entries, so
+    that the starts of each tile are written both by the lane whose entry
+    follows the run and, for long runs, by the whole wave."""
+    d, idx, val = _gap_messages(M, k, seed=M)
+    print("gaps M", M, "k", k, "d", d, flush=True)
+    w = custom(d=d, M=M, kind="topk", k=k, eta=1e-2, seed=64)
+    got = _gpu_average(w, idx, val)
+    exp = _oracle_average(w, idx, val)
+    bad = np.flatnonzero(got.view(np.uint32) != exp.view(np.uint32))
+    assert bad.size == 0, "%d of %d differ; first at %s" % (bad.size, got.size, bad[:5].tolist())
 
 
 @pytest.mark.timeout(300)
